@@ -1,0 +1,158 @@
+"""CPU oracle for the batched speculative-verification step.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg of
+the benchmark may use this package; the product path (the HIP library and its
+Python binding) never imports it, and this package never imports the product.
+
+The arithmetic lives in ``oracle.c`` (plain C, double precision), compiled with
+gcc into ``liboracle.so``.  This module only marshals numpy arrays to it.
+
+Functions (each restates the paper's definition; see ``oracle.c``):
+  attention(...)  -- softmax attention of selected (row, head) pairs against
+                     the paged KV cache (speculative verification scores all
+                     k+1 positions in one target pass, Sec. 2.2).
+  argmax(...)     -- lowest index of the row maximum, plus the top-2 gap.
+  accept(...)     -- greedy acceptance: longest matching draft prefix plus one
+                     bonus token; rejection rate = rejected / proposed (Sec. 3.1).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32 = 0
+BF16 = 1
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc (OpenMP) into liboracle.so; return its path."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.run(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"],
+            check=True,
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB)
+    i32, i64, f64, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
+    lib.oracle_attention.argtypes = [i32, i32, i32, i32, i32, i32, f64, i32, vp, vp, vp, vp,
+                                     vp, vp, i64, vp, vp, vp]
+    lib.oracle_attention.restype = ctypes.c_int
+    lib.oracle_argmax.argtypes = [i64, i64, i64, i32, vp, vp, vp]
+    lib.oracle_argmax.restype = ctypes.c_int
+    lib.oracle_accept.argtypes = [i32, vp, vp, vp, vp, vp, vp]
+    lib.oracle_accept.restype = ctypes.c_int
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _raw(a: np.ndarray, dtype_code: int) -> np.ndarray:
+    """Element storage as expected by the C side: float32, or bf16 bits as uint16."""
+    a = np.ascontiguousarray(a)
+    if dtype_code == F32:
+        if a.dtype != np.float32:
+            raise TypeError("expected float32 storage, got %s" % a.dtype)
+    else:
+        if a.dtype not in (np.uint16, np.int16):
+            raise TypeError("expected bf16 bit storage (uint16/int16), got %s" % a.dtype)
+    return a
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def attention(*, num_q_heads: int, num_kv_heads: int, head_dim: int, sliding_window: int,
+              scale: float, dtype: int, q, k_cache, v_cache, block_tables, seq_lens, q_start,
+              rows=None, heads=None) -> np.ndarray:
+    """Attention output (float64) for the given (row, head) pairs.
+
+    ``rows``/``heads`` are equal-length int arrays; both None means every pair in
+    row-major order, returned with shape [T, Hq, D]; otherwise shape [P, D].
+    """
+    lib = _load()
+    q = _raw(q, dtype)
+    k_cache = _raw(k_cache, dtype)
+    v_cache = _raw(v_cache, dtype)
+    bt = np.ascontiguousarray(block_tables, dtype=np.int32)
+    sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    qs = np.ascontiguousarray(q_start, dtype=np.int32)
+    num_seqs = sl.shape[0]
+    total_q = int(qs[-1])
+    full = rows is None and heads is None
+    if full:
+        rr, hh = np.meshgrid(np.arange(total_q, dtype=np.int32),
+                             np.arange(num_q_heads, dtype=np.int32), indexing="ij")
+        rows, heads = rr.reshape(-1), hh.reshape(-1)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    heads = np.ascontiguousarray(heads, dtype=np.int32)
+    out = np.zeros((rows.shape[0], head_dim), dtype=np.float64)
+    rc = lib.oracle_attention(num_seqs, num_q_heads, num_kv_heads, head_dim, bt.shape[1],
+                              sliding_window, float(scale), dtype, _ptr(q), _ptr(k_cache),
+                              _ptr(v_cache), _ptr(bt), _ptr(sl), _ptr(qs), rows.shape[0],
+                              _ptr(rows), _ptr(heads), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_attention rejected its arguments")
+    if full:
+        return out.reshape(total_q, num_q_heads, head_dim)
+    return out
+
+
+def argmax(logits, dtype: int, with_gap: bool = True):
+    """(argmax[int32], gap[float64] or None) for a [rows, vocab] logits array."""
+    lib = _load()
+    lg = _raw(logits, dtype)
+    rows, vocab = lg.shape
+    am = np.zeros(rows, dtype=np.int32)
+    gap = np.zeros(rows, dtype=np.float64) if with_gap else None
+    rc = lib.oracle_argmax(rows, vocab, vocab, dtype, _ptr(lg), _ptr(am),
+                           _ptr(gap) if with_gap else None)
+    if rc != 0:
+        raise ValueError("oracle_argmax rejected its arguments")
+    return am, gap
+
+
+def accept(q_start, tokens, argmax_rows):
+    """(accept_len, num_emitted, emitted) for greedy acceptance."""
+    lib = _load()
+    qs = np.ascontiguousarray(q_start, dtype=np.int32)
+    tok = np.ascontiguousarray(tokens, dtype=np.int32)
+    am = np.ascontiguousarray(argmax_rows, dtype=np.int32)
+    num_seqs = qs.shape[0] - 1
+    acc = np.zeros(num_seqs, dtype=np.int32)
+    ne = np.zeros(num_seqs, dtype=np.int32)
+    em = np.zeros(tok.shape[0], dtype=np.int32)
+    lib.oracle_accept(num_seqs, _ptr(qs), _ptr(tok), _ptr(am), _ptr(acc), _ptr(ne), _ptr(em))
+    return acc, ne, em
+
+
+def rejection_rate(accept_len, q_start):
+    """Per-request rejected / proposed drafts (NaN where no draft was proposed)."""
+    k = np.diff(np.asarray(q_start)) - 1
+    acc = np.asarray(accept_len)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        return np.where(k > 0, (k - acc) / np.maximum(k, 1), np.nan)

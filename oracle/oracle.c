@@ -1,0 +1,222 @@
+/*
+ * oracle.c -- CPU oracle for the batched speculative-verification step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may include, link or
+ * call this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark load it.  It shares no code, header, table or helper with the
+ * HIP library: the paged-cache layout, the bf16 decoding, the masks and the
+ * acceptance rule are all written out again here from their definitions.
+ *
+ * What it computes (paper: Sec. 2.2 states that speculative decoding proposes
+ * several tokens and verifies them with the target model in one pass, and that
+ * the result is identical to plain decoding; Sec. 3.1 defines the rejection
+ * rate as rejected over proposed drafts per request):
+ *
+ *   oracle_attention  -- for each requested (query row, query head) pair, the
+ *                        plain definition of causal softmax attention of that
+ *                        row against its request's paged KV cache, in double
+ *                        precision, keys visited in ascending position order.
+ *   oracle_argmax     -- per logits row, the lowest index attaining the maximum
+ *                        (plus the gap to the runner-up, for near-tie flags).
+ *   oracle_accept     -- greedy acceptance: the longest prefix of drafts equal
+ *                        to the target's argmax, followed by one bonus token.
+ *
+ * Readings of the paper that this file encodes (the paper relies on its
+ * serving engine for verification and does not spell these out):
+ *   - acceptance is greedy (argmax); ties in the argmax go to the lowest index;
+ *     a NaN anywhere in a row makes the first NaN the argmax; -0.0 == +0.0;
+ *   - query row j of a request with n scored positions and S cached keys sits
+ *     at absolute position p = S - n + j and sees keys t <= p (bottom-right
+ *     aligned causal mask inside the draft);
+ *   - a sliding window W > 0 keeps keys with p - W < t <= p;
+ *   - query head h reads KV head floor(h / (Hq / Hkv)) (grouped-query);
+ *   - scale defaults to 1/sqrt(head_dim); no soft-cap, no bias, no sinks;
+ *   - a row with no visible key (only possible when S < n) yields zeros.
+ *
+ * Paged KV layout read here (element index, x = 16 bytes / element size):
+ *   K: [num_blocks][Hkv][D/x][16][x]   -> K[t][d] of physical block b, head g
+ *      is k_cache[(((b*Hkv + g)*(D/x) + d/x)*16 + t%16)*x + d%x]
+ *   V: [num_blocks][Hkv][D][16]        -> V[t][d] = v_cache[((b*Hkv + g)*D + d)*16 + t%16]
+ *   b = block_tables[i*max_blocks_per_seq + t/16].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_F32 0
+#define ORACLE_BF16 1
+
+static double elem_to_double(const void *base, int dtype, int64_t idx)
+{
+    if (dtype == ORACLE_F32) {
+        return (double)((const float *)base)[idx];
+    }
+    /* bfloat16 is the upper half of an IEEE binary32 word. */
+    uint32_t bits = (uint32_t)((const uint16_t *)base)[idx] << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+static int elem_size(int dtype) { return dtype == ORACLE_F32 ? 4 : 2; }
+
+/* Request owning global query row `row` (q_start is an exclusive prefix sum). */
+static int find_request(int num_seqs, const int32_t *q_start, int32_t row)
+{
+    for (int i = 0; i < num_seqs; ++i)
+        if (row >= q_start[i] && row < q_start[i + 1]) return i;
+    return -1;
+}
+
+/*
+ * out[pair][d] = sum_t w_t V_t[d] / sum_t w_t,  w_t = exp(s_t - max_u s_u),
+ * s_t = scale * <q_row_head, K_t>,  t over the visible keys of the row.
+ * Returns 0, or -1 on an argument that cannot be interpreted.
+ */
+int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
+                     int32_t head_dim, int32_t max_blocks_per_seq, int32_t sliding_window,
+                     double scale, int32_t dtype, const void *q, const void *k_cache,
+                     const void *v_cache, const int32_t *block_tables,
+                     const int32_t *seq_lens, const int32_t *q_start, int64_t n_pairs,
+                     const int32_t *pair_row, const int32_t *pair_head, double *out)
+{
+    const int D = head_dim;
+    if (num_q_heads % num_kv_heads != 0) return -1;
+    const int group = num_q_heads / num_kv_heads;
+    const int x = 16 / elem_size(dtype);
+    if (D % x != 0) return -1;
+    if (scale == 0.0) scale = 1.0 / sqrt((double)D);
+    int bad = 0;
+
+#pragma omp parallel for schedule(dynamic, 4) reduction(| : bad)
+    for (int64_t pr = 0; pr < n_pairs; ++pr) {
+        const int32_t row = pair_row[pr];
+        const int32_t h = pair_head[pr];
+        double *o = out + pr * D;
+        for (int d = 0; d < D; ++d) o[d] = 0.0;
+        const int i = find_request(num_seqs, q_start, row);
+        if (i < 0 || h < 0 || h >= num_q_heads) { bad = 1; continue; }
+        const int64_t n = q_start[i + 1] - q_start[i];
+        const int64_t S = seq_lens[i];
+        const int64_t j = row - q_start[i];
+        const int64_t p = S - n + j; /* absolute position of this query row */
+        int64_t lo = 0;
+        if (sliding_window > 0 && p - sliding_window + 1 > lo) lo = p - sliding_window + 1;
+        if (p < lo || p < 0) continue; /* nothing visible: output stays zero */
+        const int g = h / group;
+
+        const int64_t nkeys = p - lo + 1;
+        double *s = (double *)malloc(sizeof(double) * nkeys);
+        if (!s) { bad = 1; continue; }
+        double smax = -INFINITY;
+        for (int64_t t = lo; t <= p; ++t) {
+            const int64_t b = block_tables[(int64_t)i * max_blocks_per_seq + t / 16];
+            double acc = 0.0;
+            for (int d = 0; d < D; ++d) {
+                const double qd = elem_to_double(q, dtype, ((int64_t)row * num_q_heads + h) * D + d);
+                const int64_t kidx =
+                    ((((int64_t)b * num_kv_heads + g) * (D / x) + d / x) * 16 + t % 16) * x + d % x;
+                acc += qd * elem_to_double(k_cache, dtype, kidx);
+            }
+            s[t - lo] = scale * acc;
+            if (s[t - lo] > smax) smax = s[t - lo];
+        }
+        double denom = 0.0;
+        for (int64_t t = lo; t <= p; ++t) {
+            const int64_t b = block_tables[(int64_t)i * max_blocks_per_seq + t / 16];
+            const double w = exp(s[t - lo] - smax);
+            denom += w;
+            for (int d = 0; d < D; ++d) {
+                const int64_t vidx = (((int64_t)b * num_kv_heads + g) * D + d) * 16 + t % 16;
+                o[d] += w * elem_to_double(v_cache, dtype, vidx);
+            }
+        }
+        for (int d = 0; d < D; ++d) o[d] /= denom;
+        free(s);
+    }
+    return bad ? -1 : 0;
+}
+
+/*
+ * argmax[r] = min { v : x[r][v] = max_u x[r][u] }  (first NaN if the row has
+ * one).  gap[r] = x[r][argmax] - max_{v != argmax} x[r][v]  (+inf for vocab 1,
+ * NaN if the row holds a NaN).  gap may be NULL.
+ */
+int oracle_argmax(int64_t rows, int64_t vocab, int64_t row_stride, int32_t dtype,
+                  const void *logits, int32_t *argmax, double *gap)
+{
+    if (vocab <= 0) return -1;
+    if (row_stride == 0) row_stride = vocab;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        const int64_t base = r * row_stride;
+        int64_t best = 0;
+        double bestv = elem_to_double(logits, dtype, base);
+        int has_nan = isnan(bestv);
+        for (int64_t v = 1; v < vocab && !has_nan; ++v) {
+            const double x = elem_to_double(logits, dtype, base + v);
+            if (isnan(x)) { best = v; bestv = x; has_nan = 1; break; }
+            if (x > bestv) { best = v; bestv = x; }
+        }
+        argmax[r] = (int32_t)best;
+        if (gap) {
+            if (has_nan) { gap[r] = NAN; continue; }
+            double second = -INFINITY;
+            for (int64_t v = 0; v < vocab; ++v) {
+                if (v == best) continue;
+                const double x = elem_to_double(logits, dtype, base + v);
+                if (x > second) second = x;
+            }
+            gap[r] = vocab == 1 ? INFINITY : bestv - second;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Greedy acceptance.  Request i owns rows q_start[i] .. q_start[i+1]-1
+ * (n_i = k_i + 1 rows).  tokens[q_start[i]] is the last committed token and
+ * tokens[q_start[i] + j] (1 <= j <= k_i) is draft j.  Row j's argmax is the
+ * target's prediction for the token after row j's input, so draft j+1 is
+ * accepted while argmax[q_start[i] + j] == tokens[q_start[i] + j + 1].
+ *   accept_len[i]  = m_i, the number of leading accepted drafts (0..k_i);
+ *   num_emitted[i] = m_i + 1 (accepted drafts plus the bonus token), or 0 for
+ *                    a request with no rows;
+ *   emitted[q_start[i] + j] = draft j+1 for j < m_i, argmax of row m_i for
+ *                    j = m_i, and -1 for the remaining rows of the request.
+ */
+int oracle_accept(int32_t num_seqs, const int32_t *q_start, const int32_t *tokens,
+                  const int32_t *argmax, int32_t *accept_len, int32_t *num_emitted,
+                  int32_t *emitted)
+{
+    for (int i = 0; i < num_seqs; ++i) {
+        const int32_t q0 = q_start[i];
+        const int32_t n = q_start[i + 1] - q0;
+        if (n <= 0) { accept_len[i] = 0; num_emitted[i] = 0; continue; }
+        const int32_t k = n - 1;
+        int32_t m = 0;
+        while (m < k && argmax[q0 + m] == tokens[q0 + m + 1]) ++m;
+        for (int32_t j = 0; j < n; ++j)
+            emitted[q0 + j] = j < m ? tokens[q0 + j + 1] : (j == m ? argmax[q0 + m] : -1);
+        accept_len[i] = m;
+        num_emitted[i] = m + 1;
+    }
+    return 0;
+}
+
+int oracle_num_threads(void)
+{
+    int n = 1;
+#ifdef _OPENMP
+#pragma omp parallel
+    {
+#pragma omp master
+        n = omp_get_num_threads();
+    }
+#endif
+    return n;
+}
