@@ -1,0 +1,233 @@
+"""Throughput of the batched speculative-verification step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3_8b]
+
+One step = every attention layer of the workload (verify_attention) followed by
+verify_accept (vocabulary argmax + greedy acceptance) over one batch of
+synthetic inputs already resident in HBM.  Prints one JSON line:
+
+  value         verified tokens/s = sum_i (accept_len_i + 1) / step time
+  roofline      the attention kernel(s): algorithmic bytes per launch / mean
+                launch time (HIP events on the launch stream) vs 8 TB/s HBM
+  cpu_baseline  the CPU oracle on a bounded sample of the same step (first
+                requests of the batch, all their heads and logits rows)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E datasheet peak
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def attention_bytes(bt, layer) -> float:
+    """Algorithmic HBM bytes of one attention layer: the visible keys' K and V
+    (union over the request's rows), Q read once, O written once, and the
+    block-table entries walked."""
+    import numpy as np
+    cfg = bt.cfg
+    e = 2 if cfg.dtype == "bf16" else 4
+    n = np.diff(bt.q_start).astype(np.int64)
+    S = bt.seq_lens.astype(np.int64)
+    vis = S if layer.window == 0 else np.minimum(S, layer.window + n - 1)
+    kv = float(vis.sum()) * 2 * cfg.num_kv_heads * cfg.head_dim * e
+    qo = 2.0 * bt.total_q * cfg.num_q_heads * cfg.head_dim * e
+    first = S - vis
+    blocks = ((S + 15) // 16 - first // 16).sum()
+    return kv + qo + 4.0 * float(blocks)
+
+
+def accept_bytes(bt) -> float:
+    cfg = bt.cfg
+    e = 2 if cfg.dtype == "bf16" else 4
+    T, B = bt.total_q, len(bt.seq_lens)
+    return float(T) * cfg.vocab * e + 4.0 * (4 * T + 3 * B + 1)
+
+
+def cpu_baseline(bt, budget_s: float):
+    """Time the oracle (as it stands) on the first requests of the batch until
+    about `budget_s` seconds of work are done; report verified tokens/s."""
+    import numpy as np
+    import oracle
+    import workload
+    cfg = bt.cfg
+    code = workload.dtype_code(cfg.dtype)
+    host = []
+    for layer in bt.layers:
+        host.append(dict(q=workload.host_storage(layer.q), k=workload.host_storage(layer.k_cache),
+                         v=workload.host_storage(layer.v_cache), window=layer.window))
+    logits = workload.host_storage(bt.logits)
+    done, emitted, elapsed = 0, 0, 0.0
+    B = len(bt.seq_lens)
+    while done < B and elapsed < budget_s:
+        i = done
+        q0, q1 = int(bt.q_start[i]), int(bt.q_start[i + 1])
+        rows = np.repeat(np.arange(q0, q1, dtype=np.int32), cfg.num_q_heads)
+        heads = np.tile(np.arange(cfg.num_q_heads, dtype=np.int32), q1 - q0)
+        t0 = time.perf_counter()
+        for h in host:
+            oracle.attention(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
+                             head_dim=cfg.head_dim, sliding_window=h["window"], scale=0.0,
+                             dtype=code, q=h["q"], k_cache=h["k"], v_cache=h["v"],
+                             block_tables=bt.block_tables, seq_lens=bt.seq_lens,
+                             q_start=bt.q_start, rows=rows, heads=heads)
+        am, _ = oracle.argmax(logits[q0:q1], code, with_gap=False)
+        qs = np.array([0, q1 - q0], dtype=np.int32)
+        acc, ne, _ = oracle.accept(qs, bt.tokens[q0:q1], am)
+        elapsed += time.perf_counter() - t0
+        emitted += int(ne[0])
+        done += 1
+    return dict(value=emitted / elapsed, unit="verified tokens/s", cores=oracle.num_threads(),
+                kind="oracle",
+                sample="first %d of %d requests (all %d heads, %d layer(s), their logits rows), "
+                       "%.1f s of CPU time" % (done, B, cfg.num_q_heads, len(bt.layers), elapsed))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="qwen3_8b")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle work for the CPU baseline (0 = skip)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the verify step runs on a single MI355X "
+              "(--gpus %d requested; multi-GPU sharding is not part of this build)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2608_24004_amd as av
+    import workload
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    cfg = workload.CONFIGS[args.config]
+    log("config", cfg.name, "seed", args.seed)
+    bt = workload.make_batch(cfg, args.seed, dev)
+    torch.cuda.synchronize()
+
+    lib = av.library()
+    stream = torch.cuda.current_stream()
+    outs = [torch.empty_like(l.q) for l in bt.layers]
+    ws = []
+    for l in bt.layers:
+        nb = av.attention_workspace_size(l.q, l.k_cache, bt.t_block_tables, max_q_len=bt.max_q_len,
+                                         max_seq_len=bt.max_seq_len, sliding_window=l.window)
+        ws.append(torch.empty(max(nb, 1), dtype=torch.uint8, device=dev))
+    T, B = bt.total_q, len(bt.seq_lens)
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    ne = torch.empty(B, dtype=torch.int32, device=dev)
+    em = torch.empty(T, dtype=torch.int32, device=dev)
+    am = torch.empty(T, dtype=torch.int32, device=dev)
+    code = workload.dtype_code(cfg.dtype)
+    aws = torch.empty(max(1, av.accept_workspace_size(B, T, cfg.vocab, code)), dtype=torch.uint8,
+                      device=dev)
+
+    def attention(li, ev=None):
+        l = bt.layers[li]
+        av.verify_attention(l.q, l.k_cache, l.v_cache, bt.t_block_tables, bt.t_seq_lens,
+                            bt.t_q_start, max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len,
+                            sliding_window=l.window, out=outs[li], workspace=ws[li])
+
+    def step(evs=None):
+        for li in range(len(bt.layers)):
+            if evs is not None:
+                evs[li][0].record(stream)
+            attention(li)
+            if evs is not None:
+                evs[li][1].record(stream)
+        av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start, argmax_out=am, accept_len=acc,
+                         num_emitted=ne, emitted=em, workspace=aws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    attn_ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+                for _ in bt.layers] for _ in range(K)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for k in range(K):
+        step(attn_ev[k])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / K
+    attn_ms = [float(np.mean([attn_ev[k][li][0].elapsed_time(attn_ev[k][li][1]) for k in range(K)]))
+               for li in range(len(bt.layers))]
+
+    emitted = int(ne.sum().item())
+    proposed = int(bt.num_drafts.sum())
+    accepted = int(acc.sum().item())
+    value = emitted / (ms_step * 1e-3)
+    # dominant kernel: the attention layer with the most algorithmic bytes
+    abytes = [attention_bytes(bt, l) for l in bt.layers]
+    dom = int(np.argmax(abytes))
+    achieved = abytes[dom] / (attn_ms[dom] * 1e-3) / 1e9
+    step_bytes = sum(abytes) + accept_bytes(bt)
+    log("step %.3f ms (wall %.3f ms), attention %s ms, accept+rest %.3f ms" % (
+        ms_step, wall / K * 1e3, ["%.3f" % x for x in attn_ms], ms_step - sum(attn_ms)))
+    log("step algorithmic bytes %.3f GB -> %.0f GB/s (%.1f%% of HBM peak); attention layer %d: "
+        "%.3f GB in %.3f ms = %.0f GB/s" % (step_bytes / 1e9, step_bytes / ms_step / 1e6,
+                                            100 * step_bytes / ms_step / 1e6 / HBM_PEAK_GBS, dom,
+                                            abytes[dom] / 1e9, attn_ms[dom], achieved))
+    log("drafts proposed %d accepted %d (rejection rate %.3f), emitted %d, scored positions %d" % (
+        proposed, accepted, 1 - accepted / max(1, proposed), emitted, T))
+
+    cpu = None
+    if args.cpu_budget > 0:
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_baseline(bt, args.cpu_budget)
+        log("cpu baseline", cpu)
+
+    res = {
+        "metric": "verified tokens/sec per verify step (1 GPU) + achieved HBM GB/s vs peak",
+        "value": value,
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "description": cfg.description, "batch": B,
+                   "total_q": T, "mean_context": float(bt.context_len.mean()),
+                   "num_q_heads": cfg.num_q_heads, "num_kv_heads": cfg.num_kv_heads,
+                   "head_dim": cfg.head_dim, "vocab": cfg.vocab, "layers": len(bt.layers),
+                   "seed": args.seed},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "verify_attention (layer %d)" % dom},
+        "step_hbm_frac": step_bytes / ms_step / 1e6 / HBM_PEAK_GBS,
+        "scored_positions_per_s": T / (ms_step * 1e-3),
+        "rejection_rate": 1 - accepted / max(1, proposed),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,160 @@
+/*
+ * agentspec_verify.h -- C ABI of the batched speculative-verification step.
+ *
+ * Speculative decoding proposes several draft tokens per request and verifies
+ * them with the target model in a single pass; the output is the same as
+ * plain decoding (paper, Sec. 2.2).  In a batch, every request i carries its
+ * own draft length k_i >= 0 (the per-request draft length L_i that the
+ * redundancy-aware allocator hands out, Sec. 4.2 / Alg. 2; k_i = 0 for a
+ * request that does not speculate), so the target scores n_i = k_i + 1
+ * positions of request i, and the step's cost grows with the number of drafts
+ * D(b) it verifies (Sec. 3.1).  The library implements that verify pass on one
+ * AMD Instinct MI355X (gfx950):
+ *
+ *   verify_attention -- the attention of all sum_i n_i query rows of one layer
+ *                       against each request's paged KV cache;
+ *   verify_accept    -- the vocabulary argmax of every scored position and
+ *                       greedy acceptance: the longest draft prefix that agrees
+ *                       with the target, plus one bonus token.  The rejection
+ *                       rate of Sec. 3.1 is (k_i - accept_len_i) / k_i.
+ *
+ * Conventions shared by both calls
+ * --------------------------------
+ *  - Requests are packed: query rows q_start[i] .. q_start[i+1]-1 (int32,
+ *    num_seqs+1 entries, q_start[0] = 0, non-decreasing) belong to request i;
+ *    total_q = q_start[num_seqs].  Row j of request i is the model input at
+ *    absolute position S_i - n_i + j, where S_i = seq_lens[i] counts the
+ *    request's cached keys including the n_i new ones (the caller writes the
+ *    new tokens' K/V into the cache before the call).
+ *  - All array pointers are device pointers owned by the caller.  The library
+ *    allocates nothing, keeps no state between calls, never reads device data
+ *    on the host, and is safe to call from several host threads on different
+ *    streams (each call with its own workspace).
+ *  - Calls are asynchronous: they validate host-side arguments, enqueue their
+ *    kernels on `stream` and return.  Device-side errors surface at the next
+ *    synchronising HIP call.
+ *  - Return value: VERIFY_OK (0) or a negative status; on a negative status
+ *    nothing was enqueued.  verify_status_string() names a status.
+ *  - Storage dtypes: VERIFY_F32 (IEEE binary32) or VERIFY_BF16 (bfloat16).
+ *    Arithmetic is fp32 (bf16 products accumulate in fp32); outputs are
+ *    rounded to the storage dtype with round-to-nearest-even.
+ */
+#ifndef AGENTSPEC_VERIFY_H
+#define AGENTSPEC_VERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum verify_status {
+    VERIFY_OK = 0,
+    VERIFY_EINVAL = -1,       /* null pointer, negative size, inconsistent arguments   */
+    VERIFY_EUNSUPPORTED = -2, /* head_dim, block_size or dtype this build does not handle */
+    VERIFY_EWORKSPACE = -3,   /* workspace smaller than the size query returned        */
+    VERIFY_EHIP = -4          /* a kernel launch failed (hipGetLastError)               */
+};
+
+enum verify_dtype { VERIFY_F32 = 0, VERIFY_BF16 = 1 };
+
+/* Shape and layout of one attention layer. */
+typedef struct verify_attn_params {
+    int32_t num_seqs;           /* requests in the batch (>= 0)                         */
+    int32_t num_q_heads;        /* Hq                                                   */
+    int32_t num_kv_heads;       /* Hkv; Hq % Hkv == 0; q-head h reads KV head h/(Hq/Hkv) */
+    int32_t head_dim;           /* D: 64 or 128                                         */
+    int32_t block_size;         /* tokens per KV block: must be 16                       */
+    int32_t max_blocks_per_seq; /* row stride of block_tables                           */
+    int32_t num_blocks;         /* physical blocks in k_cache / v_cache                 */
+    int32_t sliding_window;     /* W > 0: row at position p sees keys p-W < t <= p;
+                                   0: full causal (keys t <= p)                         */
+    float scale;                /* softmax scale; 0 selects 1/sqrt(D)                   */
+    int32_t dtype;              /* verify_dtype of q, k_cache, v_cache and out          */
+    int32_t kv_split_blocks;    /* KV blocks per split-K work item; 0 = automatic.
+                                   Results agree across splits up to fp32 rounding.     */
+} verify_attn_params;
+
+/*
+ * verify_attention -- softmax attention of every packed query row against its
+ * request's paged KV cache (the target-model scoring of Sec. 2.2, for one
+ * layer).
+ *
+ * For request i, row j (0 <= j < n_i), query head h, with p = S_i - n_i + j,
+ * g = h / (Hq/Hkv) and the visible keys t in [max(0, p-W+1), p] (W > 0) or
+ * [0, p] (W = 0):
+ *     out[row][h] = sum_t softmax_t(scale * <q[row][h], K_g[t]>) * V_g[t]
+ * where K_g[t], V_g[t] are read through block_tables[i][t / 16].
+ *
+ *   q            [total_q][Hq][D]                     (dtype)
+ *   k_cache      [num_blocks][Hkv][D/x][16][x]        x = 16 bytes / element
+ *                (token t, dim d of a block at [d/x][t][d%x])
+ *   v_cache      [num_blocks][Hkv][D][16]             (token t, dim d at [d][t])
+ *   block_tables [num_seqs][max_blocks_per_seq] int32 physical block ids; the
+ *                first ceil(S_i/16) entries of row i are read, ids outside
+ *                [0, num_blocks) are skipped (their keys contribute nothing)
+ *   seq_lens     [num_seqs] int32 S_i, with n_i <= S_i <= max_seq_len and
+ *                S_i <= 16 * max_blocks_per_seq (larger values are clamped)
+ *   q_start      [num_seqs + 1] int32
+ *   out          [total_q][Hq][D]                     (dtype); a row with no
+ *                visible key (S_i < n_i) is written as zeros
+ *   max_q_len    host upper bound on n_i; max_seq_len host upper bound on S_i
+ *                (they size the launch; tighter bounds launch less idle work)
+ *   workspace    device scratch of at least the size returned by
+ *                verify_attention_workspace_size() for the same (params,
+ *                total_q, max_q_len, max_seq_len); may be NULL if that size is
+ *                0.  Its contents on entry are ignored.
+ */
+int verify_attention_workspace_size(const verify_attn_params *params, int32_t total_q,
+                                    int32_t max_q_len, int32_t max_seq_len, size_t *bytes);
+
+int verify_attention(const verify_attn_params *params, int32_t total_q, int32_t max_q_len,
+                     int32_t max_seq_len, const void *q, const void *k_cache,
+                     const void *v_cache, const int32_t *block_tables,
+                     const int32_t *seq_lens, const int32_t *q_start, void *out,
+                     void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * verify_accept -- vocabulary argmax of each scored position and greedy
+ * acceptance of the drafts (Sec. 2.2 verification; Sec. 3.1 rejection rate).
+ *
+ *   logits      [total_q][row_stride] (logits_dtype), vocab entries per row used;
+ *               row_stride = 0 means vocab
+ *   tokens      [total_q] int32: tokens[q_start[i]] is request i's last committed
+ *               token, tokens[q_start[i] + j] (1 <= j <= k_i) is its draft j
+ *   argmax_out  [total_q] int32 or NULL: argmax_out[r] = the lowest index v with
+ *               logits[r][v] equal to the row maximum (-0.0 equals +0.0; if the
+ *               row holds a NaN, the index of its first NaN)
+ *   accept_len  [num_seqs] int32: m_i = number of leading drafts j = 1..k_i with
+ *               tokens[q_start[i] + j] == argmax[q_start[i] + j - 1]
+ *   num_emitted [num_seqs] int32: m_i + 1 (0 for a request with no rows)
+ *   emitted     [total_q] int32: request i's drafts 1..m_i, then the bonus token
+ *               argmax[q_start[i] + m_i], starting at emitted[q_start[i]]; the
+ *               request's remaining rows are set to -1
+ *   workspace   device scratch of at least verify_accept_workspace_size() bytes
+ *               (may be NULL if that is 0); its contents on entry are ignored.
+ * Requires vocab >= 1 and vocab < 2^31.
+ */
+int verify_accept_workspace_size(int32_t num_seqs, int32_t total_q, int64_t vocab,
+                                 int32_t logits_dtype, size_t *bytes);
+
+int verify_accept(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_stride,
+                  int32_t logits_dtype, const void *logits, const int32_t *tokens,
+                  const int32_t *q_start, int32_t *argmax_out, int32_t *accept_len,
+                  int32_t *num_emitted, int32_t *emitted, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char *verify_status_string(int status);
+
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int verify_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AGENTSPEC_VERIFY_H */

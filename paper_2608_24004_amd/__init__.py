@@ -1,0 +1,222 @@
+"""MI355X-native batched speculative-verification step (AgentSpec hot path).
+
+Thin ctypes binding over the C ABI in ``include/agentspec_verify.h``: argument
+marshalling only.  Every step of the verify pass runs in the HIP kernels of
+``libagentspec_verify.so``; PyTorch supplies device memory and the stream.
+If the library is missing, every entry point raises -- there is no fallback.
+
+    verify_attention(...)  paged multi-query GQA attention of all scored rows
+    verify_accept(...)     vocabulary argmax + greedy acceptance of the drafts
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+from .build import LIB_PATH
+
+__all__ = ["verify_attention", "verify_accept", "attention_workspace_size",
+           "accept_workspace_size", "VerifyError", "library", "abi_version", "F32", "BF16"]
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+F32, BF16 = 0, 1
+
+
+class VerifyError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, _status_string(status), status))
+
+
+class AttnParams(ctypes.Structure):
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int32),
+        ("sliding_window", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+        ("kv_split_blocks", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def library(path: Optional[str] = None):
+    """Load (once) and return the ctypes handle of the HIP library."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or os.environ.get("AGENTSPEC_VERIFY_LIB", LIB_PATH)
+    if not os.path.exists(path):
+        raise RuntimeError("verify library not built: %s is missing "
+                           "(run `python -m paper_2608_24004_amd.build`)" % path)
+    lib = ctypes.CDLL(path)
+    i32, i64, vp, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+    P = ctypes.POINTER(AttnParams)
+    lib.verify_attention_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.verify_attention_workspace_size.restype = ctypes.c_int
+    lib.verify_attention.argtypes = [P, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.verify_attention.restype = ctypes.c_int
+    lib.verify_accept_workspace_size.argtypes = [i32, i32, i64, i32, ctypes.POINTER(sz)]
+    lib.verify_accept_workspace_size.restype = ctypes.c_int
+    lib.verify_accept.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.verify_accept.restype = ctypes.c_int
+    lib.verify_status_string.argtypes = [ctypes.c_int]
+    lib.verify_status_string.restype = ctypes.c_char_p
+    lib.verify_abi_version.argtypes = []
+    lib.verify_abi_version.restype = ctypes.c_int
+    if path == LIB_PATH or _lib is None:
+        _lib = lib
+    return lib
+
+
+def _status_string(status: int) -> str:
+    try:
+        return library().verify_status_string(status).decode()
+    except Exception:
+        return "status %d" % status
+
+
+def abi_version() -> int:
+    return int(library().verify_abi_version())
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise VerifyError(status, where)
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError("unsupported storage dtype %s (bf16 or fp32)" % t.dtype)
+
+
+def _dev_ptr(t, name, dtype=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_ptr(stream, device):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks):
+    T, Hq, D = q.shape
+    params = AttnParams()
+    params.num_seqs = block_tables.shape[0]
+    params.num_q_heads = Hq
+    params.num_kv_heads = k_cache.shape[1]
+    params.head_dim = D
+    params.block_size = k_cache.shape[3]
+    params.max_blocks_per_seq = block_tables.shape[1]
+    params.num_blocks = k_cache.shape[0]
+    params.sliding_window = int(sliding_window)
+    params.scale = float(scale)
+    params.dtype = _dtype_code(q)
+    params.kv_split_blocks = int(kv_split_blocks)
+    return params
+
+
+def attention_workspace_size(q, k_cache, block_tables, *, max_q_len: int, max_seq_len: int,
+                             sliding_window: int = 0, scale: float = 0.0,
+                             kv_split_blocks: int = 0) -> int:
+    params = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
+    n = ctypes.c_size_t(0)
+    _check(library().verify_attention_workspace_size(ctypes.byref(params), q.shape[0], int(max_q_len),
+                                                     int(max_seq_len), ctypes.byref(n)),
+           "verify_attention_workspace_size")
+    return int(n.value)
+
+
+def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, max_q_len: int,
+                     max_seq_len: int, sliding_window: int = 0, scale: float = 0.0,
+                     kv_split_blocks: int = 0, out=None, workspace=None, stream=None):
+    """Attention of every packed query row against its request's paged KV cache.
+
+    q [T, Hq, D]; k_cache [NB, Hkv, D/x, 16, x]; v_cache [NB, Hkv, D, 16] (bf16 or
+    fp32, x = 16 bytes / element); block_tables [B, MB], seq_lens [B], q_start
+    [B+1] int32 on the device.  max_q_len / max_seq_len are host upper bounds of
+    n_i = q_start[i+1]-q_start[i] and S_i = seq_lens[i].  Returns `out`.
+    """
+    import torch
+    params = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
+    if out is None:
+        out = torch.empty_like(q)
+    ws_bytes = attention_workspace_size(q, k_cache, block_tables, max_q_len=max_q_len,
+                                        max_seq_len=max_seq_len, sliding_window=sliding_window,
+                                        scale=scale, kv_split_blocks=kv_split_blocks)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_have = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    i32 = torch.int32
+    rc = library().verify_attention(
+        ctypes.byref(params), q.shape[0], int(max_q_len), int(max_seq_len),
+        _dev_ptr(q, "q"), _dev_ptr(k_cache, "k_cache", q.dtype), _dev_ptr(v_cache, "v_cache", q.dtype),
+        _dev_ptr(block_tables, "block_tables", i32), _dev_ptr(seq_lens, "seq_lens", i32),
+        _dev_ptr(q_start, "q_start", i32), _dev_ptr(out, "out", q.dtype),
+        _dev_ptr(workspace, "workspace"), ws_have, _stream_ptr(stream, q.device))
+    _check(rc, "verify_attention")
+    return out
+
+
+def accept_workspace_size(num_seqs: int, total_q: int, vocab: int, dtype_code: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(library().verify_accept_workspace_size(int(num_seqs), int(total_q), int(vocab),
+                                                  int(dtype_code), ctypes.byref(n)),
+           "verify_accept_workspace_size")
+    return int(n.value)
+
+
+def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, num_emitted=None,
+                  emitted=None, workspace=None, stream=None):
+    """Vocabulary argmax of every row and greedy acceptance of the drafts.
+
+    logits [T, V] (bf16 or fp32), tokens [T] and q_start [B+1] int32 on the
+    device.  Returns (accept_len [B], num_emitted [B], emitted [T], argmax [T]).
+    """
+    import torch
+    T, V = logits.shape
+    B = q_start.shape[0] - 1
+    dev = logits.device
+    i32 = torch.int32
+    code = _dtype_code(logits)
+    if argmax_out is None:
+        argmax_out = torch.empty(T, dtype=i32, device=dev)
+    if accept_len is None:
+        accept_len = torch.empty(B, dtype=i32, device=dev)
+    if num_emitted is None:
+        num_emitted = torch.empty(B, dtype=i32, device=dev)
+    if emitted is None:
+        emitted = torch.empty(T, dtype=i32, device=dev)
+    ws_bytes = accept_workspace_size(B, T, V, code)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_have = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    rc = library().verify_accept(
+        B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
+        _dev_ptr(q_start, "q_start", i32), _dev_ptr(argmax_out, "argmax_out", i32),
+        _dev_ptr(accept_len, "accept_len", i32), _dev_ptr(num_emitted, "num_emitted", i32),
+        _dev_ptr(emitted, "emitted", i32), _dev_ptr(workspace, "workspace"), ws_have,
+        _stream_ptr(stream, dev))
+    _check(rc, "verify_accept")
+    return accept_len, num_emitted, emitted, argmax_out

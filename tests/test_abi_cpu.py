@@ -1,0 +1,132 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and
+rejects bad arguments with the documented status before touching the GPU."""
+from __future__ import annotations
+
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import paper_2608_24004_amd as av
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        src = open(h).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        for m in re.finditer(r"^\s*(?:const\s+)?\w+\s*\*?\s*(verify_\w+)\s*\(", src, flags=re.M):
+            names.add(m.group(1))
+    return names
+
+
+def test_header_declares_the_entry_points():
+    names = declared_symbols()
+    for n in ("verify_attention", "verify_accept", "verify_attention_workspace_size",
+              "verify_accept_workspace_size", "verify_status_string", "verify_abi_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = av.library()
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+    assert av.abi_version() == 10000
+    assert lib.verify_status_string(0) == b"ok"
+    assert lib.verify_status_string(-3) == b"workspace too small"
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    with pytest.raises(RuntimeError, match="not built"):
+        av.library(str(tmp_path / "nope.so"))
+
+
+def _params(**kw):
+    p = av.AttnParams()
+    base = dict(num_seqs=4, num_q_heads=32, num_kv_heads=8, head_dim=128, block_size=16,
+                max_blocks_per_seq=64, num_blocks=1000, sliding_window=0, scale=0.0,
+                dtype=av.BF16, kv_split_blocks=0)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(p, k, v)
+    return p
+
+
+def _ws(p, total_q=36, max_q=9, max_s=1000):
+    n = ctypes.c_size_t(0)
+    rc = av.library().verify_attention_workspace_size(ctypes.byref(p), total_q, max_q, max_s,
+                                                      ctypes.byref(n))
+    return rc, n.value
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(head_dim=96), av.EUNSUPPORTED),
+    (dict(block_size=32), av.EUNSUPPORTED),
+    (dict(dtype=7), av.EUNSUPPORTED),
+    (dict(num_q_heads=30), av.EINVAL),        # not a multiple of Hkv
+    (dict(num_kv_heads=0), av.EINVAL),
+    (dict(num_seqs=-1), av.EINVAL),
+    (dict(sliding_window=-5), av.EINVAL),
+    (dict(scale=-1.0), av.EINVAL),
+    (dict(scale=float("nan")), av.EINVAL),
+    (dict(kv_split_blocks=-2), av.EINVAL),
+    (dict(max_blocks_per_seq=0), av.EINVAL),
+])
+def test_attention_argument_validation(kw, want):
+    rc, _ = _ws(_params(**kw))
+    assert rc == want
+    # the launch entry point reports the same status (it validates first)
+    rc2 = av.library().verify_attention(ctypes.byref(_params(**kw)), 36, 9, 1000, *([None] * 7),
+                                        None, 0, None)
+    assert rc2 == want
+
+
+def test_attention_workspace_query_and_checks():
+    lib = av.library()
+    rc, n = _ws(_params(kv_split_blocks=8), total_q=36, max_q=9, max_s=1000)
+    assert rc == 0
+    # 63 blocks / 8 per split -> 8 splits: fp32 partial outputs and log-sum-exps
+    assert n >= 36 * 32 * 8 * (128 + 1) * 4
+    rc, n1 = _ws(_params(kv_split_blocks=1000), total_q=36, max_q=9, max_s=1000)
+    assert rc == 0 and n1 == 0          # one split: no workspace
+    assert lib.verify_attention_workspace_size(ctypes.byref(_params()), 36, 9, 1000, None) == av.EINVAL
+    assert lib.verify_attention_workspace_size(None, 36, 9, 1000, ctypes.byref(ctypes.c_size_t())) == av.EINVAL
+    # too small a workspace is refused before any launch (dummy non-null pointers)
+    dummy = ctypes.c_void_p(0x1000)
+    rc = lib.verify_attention(ctypes.byref(_params(kv_split_blocks=8)), 36, 9, 1000, dummy, dummy,
+                              dummy, dummy, dummy, dummy, dummy, dummy, n - 1, None)
+    assert rc == av.EWORKSPACE
+    # null required pointers
+    rc = lib.verify_attention(ctypes.byref(_params()), 36, 9, 1000, None, dummy, dummy, dummy,
+                              dummy, dummy, dummy, None, 0, None)
+    assert rc == av.EINVAL
+    # negative host sizes
+    assert _ws(_params(), total_q=-1)[0] == av.EINVAL
+    assert _ws(_params(), max_s=-1)[0] == av.EINVAL
+
+
+def test_accept_argument_validation():
+    lib = av.library()
+    n = ctypes.c_size_t(0)
+    assert lib.verify_accept_workspace_size(4, 40, 151936, av.BF16, ctypes.byref(n)) == 0
+    assert n.value >= 40 * 8
+    assert lib.verify_accept_workspace_size(4, 40, 0, av.BF16, ctypes.byref(n)) == av.EINVAL
+    assert lib.verify_accept_workspace_size(4, 40, 1 << 31, av.BF16, ctypes.byref(n)) == av.EINVAL
+    assert lib.verify_accept_workspace_size(4, 40, 100, 5, ctypes.byref(n)) == av.EUNSUPPORTED
+    assert lib.verify_accept_workspace_size(-1, 40, 100, av.F32, ctypes.byref(n)) == av.EINVAL
+    dummy = ctypes.c_void_p(0x1000)
+    args = [dummy] * 7
+    # row stride shorter than the vocabulary
+    assert lib.verify_accept(4, 40, 100, 50, av.F32, *args, dummy, 1 << 20, None) == av.EINVAL
+    # missing outputs
+    assert lib.verify_accept(4, 40, 100, 0, av.F32, dummy, dummy, dummy, dummy, None, dummy, dummy,
+                             dummy, 1 << 20, None) == av.EINVAL
+    # small workspace
+    lib.verify_accept_workspace_size(4, 40, 100, av.F32, ctypes.byref(n))
+    assert lib.verify_accept(4, 40, 100, 0, av.F32, *args, dummy, n.value - 1, None) == av.EWORKSPACE
+    # empty batch is a no-op
+    assert lib.verify_accept(0, 0, 100, 0, av.F32, *([None] * 8), 0, None) == 0

@@ -1,0 +1,239 @@
+"""GPU parity: the HIP path against the CPU oracle on the same seeded inputs.
+
+Accept: argmax, accept lengths and emitted tokens bit-exact (rows whose top-2
+gap is below 1e-3 are flagged; the generator's rows have a unique maximum, so
+the strict comparison is made on every row and the flagged count is asserted).
+Attention: per (row, head) vector within 2e-2 relative (bf16) / 1e-4 (fp32).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_24004_amd as av
+import workload
+from gpu_common import (NEAR_TIE, assert_attention_close, compact_for_rows, gpu_attention,
+                        oracle_accept_all, sample_pairs, to_host_f64)
+from helpers import Paged, random_paged
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# --------------------------------------------------------------------------- accept
+
+
+@pytest.mark.parametrize("name", list(workload.CONFIGS))
+def test_accept_full_size(name):
+    cfg = workload.CONFIGS[name]
+    say("accept full", name)
+    bt = workload.make_batch(cfg, 0, DEV, with_layers=False)
+    acc, ne, em, am = av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start)
+    torch.cuda.synchronize()
+    r_am, gap, r_acc, r_ne, r_em = oracle_accept_all(bt.logits, bt.q_start, bt.tokens,
+                                                     workload.dtype_code(cfg.dtype))
+    assert int((gap < NEAR_TIE).sum()) == 0
+    np.testing.assert_array_equal(am.cpu().numpy(), r_am)
+    np.testing.assert_array_equal(acc.cpu().numpy(), r_acc)
+    np.testing.assert_array_equal(ne.cpu().numpy(), r_ne)
+    np.testing.assert_array_equal(em.cpu().numpy(), r_em)
+
+
+def _accept_case(rows_per_req, vocab, dtype, fill, seed):
+    rng = np.random.default_rng(seed)
+    n = np.asarray(rows_per_req)
+    q_start = np.zeros(n.size + 1, dtype=np.int32)
+    q_start[1:] = np.cumsum(n)
+    T = int(q_start[-1])
+    vals = fill(rng, (T, vocab)).astype(np.float32)
+    logits = torch.as_tensor(vals).to(workload.torch_dtype(dtype))
+    host = workload.host_storage(logits)
+    am_ref, _ = oracle.argmax(host, workload.dtype_code(dtype), with_gap=False)
+    # plant long accepted runs so the scan crosses 64-row chunks
+    tokens = rng.integers(0, vocab, size=T).astype(np.int32)
+    for i in range(n.size):
+        q0 = q_start[i]
+        J = int(rng.integers(0, max(1, n[i])))
+        for j in range(max(0, n[i] - 1)):
+            if j < J:
+                tokens[q0 + j + 1] = am_ref[q0 + j]
+    return logits, tokens, q_start
+
+
+def _ties(rng, shape):
+    return rng.integers(-3, 4, size=shape)
+
+
+def _specials(rng, shape):
+    x = rng.standard_normal(shape)
+    T, V = shape
+    for r in range(T):
+        kind = r % 6
+        if kind == 0:
+            x[r, rng.integers(0, V, size=2)] = np.nan
+        elif kind == 1:
+            x[r] = -np.inf
+        elif kind == 2:
+            x[r] = -np.abs(x[r]) - 1
+            x[r, rng.integers(0, V)] = -0.0
+            x[r, rng.integers(0, V)] = 0.0
+        elif kind == 3:
+            x[r, rng.integers(0, V, size=3)] = np.inf
+        elif kind == 4:
+            x[r] = 0.0
+    return x
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("vocab", [1, 7, 8, 1000, 8193, 40000, 151936])
+@pytest.mark.parametrize("fill", [_ties, _specials], ids=["ties", "specials"])
+def test_accept_edge_cases(dtype, vocab, fill):
+    rows = [1, 3, 0, 9, 70, 1, 33, 0, 2]   # includes empty requests and > 64 rows
+    if vocab >= 40000:
+        rows = [1, 70, 0, 5]
+    logits, tokens, q_start = _accept_case(rows, vocab, dtype, fill, seed=vocab)
+    say("accept edge", dtype, vocab, fill.__name__)
+    acc, ne, em, am = av.verify_accept(logits.to(DEV), torch.as_tensor(tokens, device=DEV),
+                                       torch.as_tensor(q_start, device=DEV))
+    torch.cuda.synchronize()
+    r_am, _, r_acc, r_ne, r_em = oracle_accept_all(logits, q_start, tokens,
+                                                   workload.dtype_code(dtype))
+    np.testing.assert_array_equal(am.cpu().numpy(), r_am)
+    np.testing.assert_array_equal(acc.cpu().numpy(), r_acc)
+    np.testing.assert_array_equal(ne.cpu().numpy(), r_ne)
+    np.testing.assert_array_equal(em.cpu().numpy(), r_em)
+
+
+def test_accept_strided_rows():
+    # logits rows with padding after the vocabulary (row stride > vocab)
+    V, stride = 1000, 1024
+    full = torch.randn(40, stride, device=DEV).to(torch.bfloat16)
+    view = full[:, :V]
+    q_start = torch.tensor([0, 9, 40], dtype=torch.int32, device=DEV)
+    tokens = torch.randint(0, V, (40,), dtype=torch.int32, device=DEV)
+    lib = av.library()
+    import ctypes
+    am = torch.empty(40, dtype=torch.int32, device=DEV)
+    acc = torch.empty(2, dtype=torch.int32, device=DEV)
+    ne = torch.empty(2, dtype=torch.int32, device=DEV)
+    em = torch.empty(40, dtype=torch.int32, device=DEV)
+    nbytes = av.accept_workspace_size(2, 40, V, av.BF16)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    p = lambda t: ctypes.c_void_p(t.data_ptr())
+    rc = lib.verify_accept(2, 40, V, stride, av.BF16, p(full), p(tokens), p(q_start), p(am), p(acc),
+                           p(ne), p(em), p(ws), nbytes,
+                           ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert rc == 0
+    torch.cuda.synchronize()
+    ref, _ = oracle.argmax(workload.host_storage(view.contiguous()), av.BF16, with_gap=False)
+    np.testing.assert_array_equal(am.cpu().numpy(), ref)
+
+
+# --------------------------------------------------------------------------- attention
+
+
+def _to_dev(p: Paged):
+    return dict(q=p.q.to(DEV), kc=p.k_cache.to(DEV), vc=p.v_cache.to(DEV),
+                bt=torch.as_tensor(p.block_tables, device=DEV),
+                sl=torch.as_tensor(p.seq_lens, device=DEV),
+                qs=torch.as_tensor(p.q_start, device=DEV))
+
+
+def _check_paged(p: Paged, split=0, what=""):
+    d = _to_dev(p)
+    out = gpu_attention(d["q"], d["kc"], d["vc"], d["bt"], d["sl"], d["qs"],
+                        max_q_len=int(np.diff(p.q_start).max()), max_seq_len=int(p.seq_lens.max()),
+                        window=p.window, split=split)
+    ref = oracle.attention(**p.oracle_args())
+    return assert_attention_close(to_host_f64(out), ref, p.dtype, what)
+
+
+SHAPES = [(8, 2, 64), (32, 8, 128), (64, 8, 64), (4, 4, 128), (8, 1, 128), (16, 2, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("hq,hkv,d", SHAPES)
+@pytest.mark.parametrize("window", [0, 5, 128])
+def test_attention_ragged_small(dtype, hq, hkv, d, window):
+    rng = np.random.default_rng(hq * 7 + d + window)
+    drafts = [0, 1, 2, 4, 8, 16, 32, 3, 0, 7]
+    contexts = [0, 1, 15, 16, 31, 200, 600, 47, 333, 129]
+    rng.shuffle(drafts)
+    say("attn ragged", dtype, hq, hkv, d, window)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                     contexts=contexts, drafts=drafts, window=window, seed=int(rng.integers(1 << 30)))
+    for split in (0, 1, 3):
+        _check_paged(p, split=split, what="split=%d" % split)
+
+
+@pytest.mark.parametrize("k", list(range(0, 33)))
+def test_attention_every_draft_length(k):
+    say("attn k", k)
+    p = random_paged(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype="bf16",
+                     contexts=[5, 100, 517], drafts=[k, k, k], seed=k)
+    _check_paged(p, split=4)
+
+
+def test_attention_spiky_masks():
+    # Large-norm queries and a planted key that matches them at a position just
+    # after some rows: a causal or window leak changes those rows by O(1).
+    rng = np.random.default_rng(9)
+    Hq, Hkv, D = 8, 2, 128
+    for window in (0, 24):
+        ctx, k = [60, 33], [12, 20]
+        k_log, v_log = [], []
+        for L, kk in zip(ctx, k):
+            S = L + kk + 1
+            K = rng.standard_normal((S, Hkv, D)) * 0.1
+            V = rng.standard_normal((S, Hkv, D))
+            K[S - 3] = 3.0          # huge score for every query pointing along +1
+            V[S - 3] = 50.0
+            if window:
+                K[S - kk - 1 - window] = 3.0   # just outside the first row's window
+                V[S - kk - 1 - window] = -50.0
+            k_log.append(K)
+            v_log.append(V)
+        T = sum(kk + 1 for kk in k)
+        q = np.abs(rng.standard_normal((T, Hq, D))) * 3.0
+        p = Paged(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, dtype="bf16", k_logical=k_log,
+                  v_logical=v_log, q=q, num_drafts=k, window=window, seed=3)
+        for split in (0, 1, 2):
+            _check_paged(p, split=split, what="spiky w=%d split=%d" % (window, split))
+
+
+def test_attention_split_invariance_and_degenerate():
+    # one request with no context (S = n), single keys, and requests of all sizes
+    p = random_paged(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype="bf16",
+                     contexts=[0, 0, 1, 2000, 4000], drafts=[0, 5, 0, 9, 1], seed=77)
+    for split in (0, 1, 2, 5, 16, 64, 1000):
+        say("attn split", split)
+        _check_paged(p, split=split, what="split=%d" % split)
+
+
+@pytest.mark.parametrize("name", list(workload.CONFIGS))
+def test_attention_full_size_sampled(name):
+    cfg = workload.CONFIGS[name]
+    say("attn full", name)
+    bt = workload.make_batch(cfg, 0, DEV, with_logits=False)
+    rows, heads = sample_pairs(bt, 160, seed=1)
+    for layer in bt.layers:
+        out = gpu_attention(layer.q, layer.k_cache, layer.v_cache, bt.t_block_tables,
+                            bt.t_seq_lens, bt.t_q_start, max_q_len=bt.max_q_len,
+                            max_seq_len=bt.max_seq_len, window=layer.window)
+        got = to_host_f64(out[torch.as_tensor(rows, device=DEV, dtype=torch.int64),
+                              torch.as_tensor(heads, device=DEV, dtype=torch.int64)])
+        args, rows_c = compact_for_rows(bt, layer, rows)
+        ref = oracle.attention(rows=rows_c, heads=heads, **args)
+        err = assert_attention_close(got, ref, cfg.dtype, "%s window=%d" % (name, layer.window))
+        say("  window", layer.window, "max rel err", err)
+        assert torch.isfinite(out.float()).all()
+        del out
+    torch.cuda.empty_cache()

@@ -332,12 +332,14 @@ def _randn_storage(shape, g, device, dt, chunk_elems: int = 1 << 28):
 
 def pack_request_kv(k_logical, v_logical, block_row: np.ndarray, k_cache, v_cache, kv_head: int):
     """Write one request's logical K/V ([S, D] tensors, one KV head) into the paged caches."""
+    import torch
     S, D = k_logical.shape
     x = k_cache.shape[-1]
-    for t in range(S):
-        b = int(block_row[t // BLOCK])
-        k_cache[b, kv_head, :, t % BLOCK, :] = k_logical[t].reshape(D // x, x)
-        v_cache[b, kv_head, :, t % BLOCK] = v_logical[t]
+    t = torch.arange(S)
+    b = torch.as_tensor(np.asarray(block_row)[(t // BLOCK).numpy()], dtype=torch.int64)
+    o = t % BLOCK
+    k_cache[b, kv_head, :, o, :] = k_logical.reshape(S, D // x, x).to(k_cache.dtype)
+    v_cache[b, kv_head, :, o] = v_logical.to(v_cache.dtype)
 
 
 def host_storage(t) -> np.ndarray:
