@@ -55,8 +55,11 @@ def accept_bytes(bt) -> float:
 
 
 def cpu_baseline(bt, budget_s: float):
-    """Time the oracle (as it stands) on the first requests of the batch until
-    about `budget_s` seconds of work are done; report verified tokens/s."""
+    """Time the oracle (as it stands) on the same step: request by request, all
+    heads, every layer, and the request's logits rows, until the whole batch is
+    done or about `budget_s` seconds have passed.  If the whole batch takes less
+    than that, the pass is repeated (up to 5 times) and the median pass is used.
+    Reports verified tokens/s of the processed requests."""
     import numpy as np
     import oracle
     import workload
@@ -67,30 +70,39 @@ def cpu_baseline(bt, budget_s: float):
         host.append(dict(q=workload.host_storage(layer.q), k=workload.host_storage(layer.k_cache),
                          v=workload.host_storage(layer.v_cache), window=layer.window))
     logits = workload.host_storage(bt.logits)
-    done, emitted, elapsed = 0, 0, 0.0
     B = len(bt.seq_lens)
-    while done < B and elapsed < budget_s:
-        i = done
-        q0, q1 = int(bt.q_start[i]), int(bt.q_start[i + 1])
-        rows = np.repeat(np.arange(q0, q1, dtype=np.int32), cfg.num_q_heads)
-        heads = np.tile(np.arange(cfg.num_q_heads, dtype=np.int32), q1 - q0)
-        t0 = time.perf_counter()
-        for h in host:
-            oracle.attention(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
-                             head_dim=cfg.head_dim, sliding_window=h["window"], scale=0.0,
-                             dtype=code, q=h["q"], k_cache=h["k"], v_cache=h["v"],
-                             block_tables=bt.block_tables, seq_lens=bt.seq_lens,
-                             q_start=bt.q_start, rows=rows, heads=heads)
-        am, _ = oracle.argmax(logits[q0:q1], code, with_gap=False)
-        qs = np.array([0, q1 - q0], dtype=np.int32)
-        acc, ne, _ = oracle.accept(qs, bt.tokens[q0:q1], am)
-        elapsed += time.perf_counter() - t0
-        emitted += int(ne[0])
-        done += 1
-    return dict(value=emitted / elapsed, unit="verified tokens/s", cores=oracle.num_threads(),
-                kind="oracle",
-                sample="first %d of %d requests (all %d heads, %d layer(s), their logits rows), "
-                       "%.1f s of CPU time" % (done, B, cfg.num_q_heads, len(bt.layers), elapsed))
+    passes = []
+    spent = 0.0
+    while spent < budget_s and len(passes) < 5:
+        done, emitted, elapsed = 0, 0, 0.0
+        while done < B and spent + elapsed < budget_s * 2:
+            i = done
+            q0, q1 = int(bt.q_start[i]), int(bt.q_start[i + 1])
+            rows = np.repeat(np.arange(q0, q1, dtype=np.int32), cfg.num_q_heads)
+            heads = np.tile(np.arange(cfg.num_q_heads, dtype=np.int32), q1 - q0)
+            t0 = time.perf_counter()
+            for h in host:
+                oracle.attention(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
+                                 head_dim=cfg.head_dim, sliding_window=h["window"], scale=0.0,
+                                 dtype=code, q=h["q"], k_cache=h["k"], v_cache=h["v"],
+                                 block_tables=bt.block_tables, seq_lens=bt.seq_lens,
+                                 q_start=bt.q_start, rows=rows, heads=heads)
+            am, _ = oracle.argmax(logits[q0:q1], code, with_gap=False)
+            qs = np.array([0, q1 - q0], dtype=np.int32)
+            acc, ne, _ = oracle.accept(qs, bt.tokens[q0:q1], am)
+            elapsed += time.perf_counter() - t0
+            emitted += int(ne[0])
+            done += 1
+        spent += elapsed
+        passes.append((emitted / elapsed, done, elapsed))
+        if done < B:
+            break
+    passes.sort()
+    value, done, elapsed = passes[len(passes) // 2]
+    return dict(value=value, unit="verified tokens/s", cores=oracle.num_threads(), kind="oracle",
+                sample="%d of %d requests (all %d heads, %d layer(s), their logits rows); "
+                       "median of %d pass(es), %.2f s per pass" % (
+                           done, B, cfg.num_q_heads, len(bt.layers), len(passes), elapsed))
 
 
 def main():

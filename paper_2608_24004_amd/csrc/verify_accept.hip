@@ -43,13 +43,17 @@ __device__ __forceinline__ bool any_nan_f32x4(const uint4& v) {
     return ((v.x & m) > inf) | ((v.y & m) > inf) | ((v.z & m) > inf) | ((v.w & m) > inf);
 }
 
+constexpr uint32_t kNone = 0xffffffffu;  // no element recorded
+
 // Scan one 16-byte vector of E elements starting at element index `base`.
 // Keeps the first strict maximum in ascending index order (float compare:
-// -0.0 == +0.0), so ties inside a thread go to the lower index.  Vectors with
-// a NaN take the exact key path.
+// -0.0 == +0.0), so ties inside a thread go to the lower index.  A vector with
+// a NaN only records the index of its first NaN (a thread scans ascending
+// indices, so the first NaN it records is its lowest); finite maxima are then
+// irrelevant for the row.
 template <typename T>
 __device__ __forceinline__ void scan_vec(const uint4& v, uint32_t base, float& best,
-                                         uint32_t& best_idx, bool& best_nan) {
+                                         uint32_t& best_idx, uint32_t& nan_idx) {
     constexpr int E = Storage<T>::kPer16B;
     float x[E];
     unpack16(v, x, T());
@@ -61,10 +65,10 @@ __device__ __forceinline__ void scan_vec(const uint4& v, uint32_t base, float& b
             best = gt ? x[e] : best;
             best_idx = gt ? base + e : best_idx;
         }
-    } else if (!best_nan) {
+    } else if (nan_idx == kNone) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            if (x[e] != x[e]) { best_nan = true; best_idx = base + e; break; }
+            if (x[e] != x[e]) { nan_idx = base + e; break; }
         }
     }
 }
@@ -82,8 +86,8 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_chunks(
     const int tid = threadIdx.x;
 
     float best = -INFINITY;
-    uint32_t best_idx = 0xffffffffu;  // "nothing seen"
-    bool best_nan = false;
+    uint32_t best_idx = kNone;  // first strict finite/inf maximum seen
+    uint32_t nan_idx = kNone;   // first NaN seen
 
     if ((reinterpret_cast<uintptr_t>(rowp + lo) & 15u) == 0) {
         const uint4* vp = reinterpret_cast<const uint4*>(rowp + lo);
@@ -95,23 +99,23 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_chunks(
             for (int u = 0; u < kArgmaxUnroll; ++u) v[u] = ld16_stream(vp + vi + u * kArgmaxThreads);
 #pragma unroll
             for (int u = 0; u < kArgmaxUnroll; ++u)
-                scan_vec<T>(v[u], (uint32_t)(lo + (vi + u * kArgmaxThreads) * E), best, best_idx, best_nan);
+                scan_vec<T>(v[u], (uint32_t)(lo + (vi + u * kArgmaxThreads) * E), best, best_idx, nan_idx);
         }
         for (; vi < nvec; vi += kArgmaxThreads) {
             uint4 v = ld16_stream(vp + vi);
-            scan_vec<T>(v, (uint32_t)(lo + vi * E), best, best_idx, best_nan);
+            scan_vec<T>(v, (uint32_t)(lo + vi * E), best, best_idx, nan_idx);
         }
         for (int64_t e = lo + nvec * E + tid; e < hi; e += kArgmaxThreads) {
             const float x = Storage<T>::load(rowp, e);
             if (x != x) {
-                if (!best_nan) { best_nan = true; best_idx = (uint32_t)e; }
+                if (nan_idx == kNone) nan_idx = (uint32_t)e;
             } else if (x > best) { best = x; best_idx = (uint32_t)e; }
         }
     } else {
         for (int64_t e = lo + tid; e < hi; e += kArgmaxThreads) {
             const float x = Storage<T>::load(rowp, e);
             if (x != x) {
-                if (!best_nan) { best_nan = true; best_idx = (uint32_t)e; }
+                if (nan_idx == kNone) nan_idx = (uint32_t)e;
             } else if (x > best) { best = x; best_idx = (uint32_t)e; }
         }
     }
@@ -119,9 +123,9 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_chunks(
     // Threads that saw only -inf report nothing, except thread 0, which owns
     // the chunk's first element: an all -inf chunk reports its lowest index.
     uint64_t packed = 0;
-    if (best_nan) {
-        packed = pack(0xffffffffu, best_idx);
-    } else if (best_idx != 0xffffffffu) {
+    if (nan_idx != kNone) {
+        packed = pack(0xffffffffu, nan_idx);
+    } else if (best_idx != kNone) {
         packed = pack(order_key(__float_as_uint(best)), best_idx);
     } else if (tid == 0 && lo < hi) {
         packed = pack(order_key(__float_as_uint(-INFINITY)), (uint32_t)lo);
