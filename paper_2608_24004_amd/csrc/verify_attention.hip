@@ -225,6 +225,233 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ MFMA path (bf16)
+//
+// Work item as for the VALU path, with up to NW*TPW*16 rows.  The workgroup's
+// NW wavefronts split the query rows (TPW tiles of 16 rows each) and share the
+// KV blocks: every block's K and V tiles (16 tokens x D, contiguous in the
+// paged layout) are loaded once per workgroup with 16-byte coalesced loads,
+// staged through a double-buffered LDS ring, and read by every wavefront as
+// MFMA operands.  Two blocks are in flight in registers while the current one
+// is consumed.
+//
+// Per block and 16-row tile, with lane = 16*lg + l16:
+//   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K (16 keys x 32 dims, lane
+//                 holds 8 consecutive dims of key l16: one 16-byte LDS read
+//                 of the x-packed K tile), B = Q^T (8 dims of row l16);
+//                 result lane holds keys 4lg..4lg+3 of row l16;
+//   O^T += V^T P^T v_mfma_f32_16x16x16_bf16, A = V^T (dims x 16 keys, lane
+//                 holds 4 keys of dim l16: one 8-byte read of the V^T tile),
+//                 B = P^T (the same 4 keys of row l16, straight from the S
+//                 registers after the online-softmax update).
+// The output tile is O^T: lane holds dims 4lg..4lg+3 of row l16, so a row's
+// state (running max, rescale factor) lives in the lanes that own its scores.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+template <int D, int NW, int TPW>
+__global__ __launch_bounds__(NW * kWave) void attn_mfma(AttnArgs a) {
+    constexpr int NT = NW * kWave;
+    constexpr int TILE_BYTES = kBlockTokens * D * 2;  // one (block, head) K or V tile
+    constexpr int CH = 2 * TILE_BYTES / 16;           // 16-byte chunks per block (K then V)
+    constexpr int CPT = (CH + NT - 1) / NT;           // chunks per thread per block
+    constexpr int KC = D / 32;                        // QK^T steps of 32 dims
+    constexpr int DT = D / 16;                        // PV output tiles of 16 dims
+    constexpr int ROWS = NW * TPW * 16;
+
+    __shared__ __attribute__((aligned(16))) uint8_t stage[2][2 * TILE_BYTES];
+
+    const int i = blockIdx.z;
+    const int kvh = blockIdx.y / a.row_groups;
+    const int rg = blockIdx.y - kvh * a.row_groups;
+    const int s = blockIdx.x;
+    const SeqGeom sg = seq_geom(a, i);
+    const int rows_total = a.group * sg.n;
+    const int r0 = rg * ROWS;
+    if (r0 >= rows_total || s >= sg.nsplit) return;
+    const int sb = sg.b_lo + s * a.split_blocks;
+    const int se = min(sg.b_hi, sb + a.split_blocks);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int w = tid / kWave;
+    const int l16 = lane & 15, lg = lane >> 4;
+    const int wrow0 = r0 + w * TPW * 16;          // first row of this wavefront
+    const bool active = wrow0 < rows_total;       // wavefront-uniform
+
+    // Q operands of this lane's rows (zeros for padding rows)
+    bf16x8_t qop[TPW][KC];
+    int row_j[TPW];
+    const uint16_t* qp = static_cast<const uint16_t*>(a.q);
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+        const int rr = wrow0 + t * 16 + l16;
+        const bool valid = rr < rows_total;
+        const int j = rr / a.group, gh = rr - j * a.group;
+        row_j[t] = valid ? j : -1;
+        const int64_t base = ((int64_t)(sg.q0 + j) * a.hq + kvh * a.group + gh) * D;
+#pragma unroll
+        for (int cc = 0; cc < KC; ++cc) {
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (valid) v = ld16(qp + base + (cc * 4 + lg) * 8);
+            qop[t][cc] = as_bf16x8(v);
+        }
+    }
+
+    f32x4_t o[TPW][DT];
+    float m_r[TPW], l_r[TPW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+        m_r[t] = -INFINITY;
+        l_r[t] = 0.f;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+
+    const uint8_t* kbase = static_cast<const uint8_t*>(a.kc);
+    const uint8_t* vbase = static_cast<const uint8_t*>(a.vc);
+    const int32_t* btab = a.block_tables + (int64_t)i * a.max_blocks;
+    const int p_first = sg.S - sg.n;   // position of the request's first query row
+
+    auto load_block = [&](int b, uint4* regs) {
+        const int phys = btab[b];
+        if (phys < 0 || phys >= a.num_blocks) return;
+        const int64_t off = ((int64_t)phys * a.hkv + kvh) * TILE_BYTES;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            const int idx = tid + c * NT;
+            if (CH % NT == 0 || idx < CH) {
+                const uint8_t* src = idx < CH / 2 ? kbase + off + idx * 16 : vbase + off + (idx - CH / 2) * 16;
+                regs[c] = ld16(src);
+            }
+        }
+    };
+    auto store_block = [&](int st, const uint4* regs) {
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            const int idx = tid + c * NT;
+            if (CH % NT == 0 || idx < CH) *reinterpret_cast<uint4*>(&stage[st][idx * 16]) = regs[c];
+        }
+    };
+    auto compute = [&](int st, int b) {
+        const int phys = btab[b];
+        if (!active || phys < 0 || phys >= a.num_blocks) return;
+        const uint8_t* ks = stage[st];
+        const uint8_t* vs = stage[st] + TILE_BYTES;
+        f32x4_t sacc[TPW];
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int cc = 0; cc < KC; ++cc) {
+            const bf16x8_t kop = as_bf16x8(*reinterpret_cast<const uint4*>(ks + ((cc * 4 + lg) * 16 + l16) * 16));
+#pragma unroll
+            for (int t = 0; t < TPW; ++t)
+                sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[t][cc], sacc[t], 0, 0, 0);
+        }
+        const int key0 = b * kBlockTokens + 4 * lg;
+        // blocks entirely below the first row's position and inside the last
+        // row's window need no mask
+        const bool need_mask = (b * kBlockTokens + kBlockTokens - 1 > p_first) ||
+                               (a.window > 0 && b * kBlockTokens < sg.S - a.window);
+        i16x4_t pop[TPW];
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            float sv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sv[r] = sacc[t][r] * a.scale_log2;
+            if (need_mask) {
+                const int p = p_first + row_j[t];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int key = key0 + r;
+                    const bool vis = row_j[t] >= 0 && key <= p && (a.window == 0 || key > p - a.window);
+                    sv[r] = vis ? sv[r] : -INFINITY;
+                }
+            }
+            float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float mnew = fmaxf(m_r[t], mx);
+            const float muse = mnew == -INFINITY ? 0.f : mnew;
+            const float alpha = exp2f(m_r[t] - muse);
+            float pr[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) pr[r] = exp2f(sv[r] - muse);
+            l_r[t] = l_r[t] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
+            m_r[t] = mnew;
+            const uint32_t lo = pack_bf16x2(pr[0], pr[1]), hi = pack_bf16x2(pr[2], pr[3]);
+            pop[t] = __builtin_bit_cast(i16x4_t, make_uint2(lo, hi));
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const uint2 vv = *reinterpret_cast<const uint2*>(vs + (dt * 16 + l16) * 32 + lg * 8);
+            const i16x4_t vop = __builtin_bit_cast(i16x4_t, vv);
+#pragma unroll
+            for (int t = 0; t < TPW; ++t)
+                o[t][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop[t], o[t][dt], 0, 0, 0);
+        }
+    };
+
+    // double-buffered LDS ring fed by two register sets
+    uint4 pa[CPT], pb[CPT];
+    if (sb < se) load_block(sb, pa);
+    if (sb + 1 < se) load_block(sb + 1, pb);
+    if (sb < se) store_block(0, pa);
+    if (sb + 2 < se) load_block(sb + 2, pa);
+    __syncthreads();
+    for (int b = sb; b < se; b += 2) {
+        compute(0, b);
+        if (b + 1 < se) store_block(1, pb);
+        if (b + 3 < se) load_block(b + 3, pb);
+        __syncthreads();
+        if (b + 1 >= se) break;
+        compute(1, b + 1);
+        if (b + 2 < se) store_block(0, pa);
+        if (b + 4 < se) load_block(b + 4, pa);
+        __syncthreads();
+    }
+
+    if (!active) return;
+    uint16_t* outp = static_cast<uint16_t*>(a.out);
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+        float L = l_r[t];
+        L += __shfl_xor(L, 16);
+        L += __shfl_xor(L, 32);
+        const int rr = wrow0 + t * 16 + l16;
+        if (rr >= rows_total) continue;
+        const int j = rr / a.group, gh = rr - j * a.group;
+        const int64_t hrow = (int64_t)(sg.q0 + j) * a.hq + kvh * a.group + gh;
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        if (sg.nsplit == 1) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const int d0 = dt * 16 + 4 * lg;
+                const uint2 v = make_uint2(pack_bf16x2(o[t][dt][0] * inv, o[t][dt][1] * inv),
+                                           pack_bf16x2(o[t][dt][2] * inv, o[t][dt][3] * inv));
+                *reinterpret_cast<uint2*>(outp + hrow * D + d0) = v;
+            }
+        } else {
+            const int64_t pi = hrow * a.max_splits + s;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const int d0 = dt * 16 + 4 * lg;
+                *reinterpret_cast<f32x4_t*>(a.part_o + pi * D + d0) = o[t][dt] * inv;
+            }
+            if (lg == 0) a.part_lse[pi] = L > 0.f ? m_r[t] + log2f(L) : -INFINITY;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ combine
 //
 // One wavefront per (query row, q-head): log-sum-exp merge of the split
@@ -274,6 +501,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_combine(AttnArgs a, int tot
 // ------------------------------------------------------------------ host side
 
 struct AttnPlan {
+    bool mfma;        // bf16 storage: MFMA kernel; fp32 storage: VALU kernel
+    int nw, tpw;      // MFMA: wavefronts per workgroup, 16-row tiles per wavefront
     int split_blocks;
     int max_splits;
     int row_groups;
@@ -308,8 +537,7 @@ AttnPlan make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_l
     nb_max = std::max<int64_t>(nb_max, 1);
     int sb = p->kv_split_blocks;
     if (sb == 0) {
-        // aim for about 8192 work items over the batch, in multiples of the
-        // four wavefronts of a workgroup, at least 32 blocks per split
+        // aim for about 8192 work items over the batch, at least 32 blocks per split
         const int64_t total = (int64_t)std::max(1, p->num_seqs) * p->num_kv_heads * nb_max;
         int64_t want = (total + 8191) / 8192;
         want = std::max<int64_t>(32, (want + 3) / 4 * 4);
@@ -318,7 +546,17 @@ AttnPlan make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_l
     pl.split_blocks = std::max(1, sb);
     pl.max_splits = (int)((nb_max + pl.split_blocks - 1) / pl.split_blocks);
     const int64_t rows = (int64_t)G * std::max(1, max_q_len);
-    pl.row_groups = (int)((rows + kValuRows - 1) / kValuRows);
+    pl.mfma = p->dtype == VERIFY_BF16;
+    if (pl.mfma) {
+        const int64_t tiles = (rows + 15) / 16;
+        if (tiles <= 8) { pl.tpw = 1; pl.nw = (int)std::max<int64_t>(2, tiles); }
+        else if (tiles <= 16) { pl.tpw = 2; pl.nw = (int)((tiles + 1) / 2); }
+        else { pl.tpw = 2; pl.nw = 8; }
+        const int64_t per = (int64_t)pl.nw * pl.tpw * 16;
+        pl.row_groups = (int)((rows + per - 1) / per);
+    } else {
+        pl.row_groups = (int)((rows + kValuRows - 1) / kValuRows);
+    }
     if (pl.max_splits > 1) {
         const size_t items = (size_t)total_q * p->num_q_heads * pl.max_splits;
         pl.part_o_bytes = align_up(items * p->head_dim * sizeof(float), 256);
@@ -327,15 +565,52 @@ AttnPlan make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_l
     return pl;
 }
 
-template <typename T, int D>
-void launch(const AttnArgs& a, const AttnPlan& pl, int total_q, hipStream_t stream) {
+template <int D, int NW, int TPW>
+void launch_mfma_k(const AttnArgs& a, const AttnPlan& pl, hipStream_t stream) {
     dim3 grid(pl.max_splits, a.hkv * pl.row_groups, a.num_seqs);
-    hipLaunchKernelGGL((attn_valu<T, D>), grid, dim3(kAttnThreads), 0, stream, a);
+    hipLaunchKernelGGL((attn_mfma<D, NW, TPW>), grid, dim3(NW * kWave), 0, stream, a);
+}
+
+template <int D>
+void launch_mfma(const AttnArgs& a, const AttnPlan& pl, hipStream_t stream) {
+    if (pl.tpw == 1) {
+        switch (pl.nw) {
+            case 2: launch_mfma_k<D, 2, 1>(a, pl, stream); break;
+            case 3: launch_mfma_k<D, 3, 1>(a, pl, stream); break;
+            case 4: launch_mfma_k<D, 4, 1>(a, pl, stream); break;
+            case 5: launch_mfma_k<D, 5, 1>(a, pl, stream); break;
+            case 6: launch_mfma_k<D, 6, 1>(a, pl, stream); break;
+            case 7: launch_mfma_k<D, 7, 1>(a, pl, stream); break;
+            default: launch_mfma_k<D, 8, 1>(a, pl, stream); break;
+        }
+    } else {
+        switch (pl.nw) {
+            case 5: launch_mfma_k<D, 5, 2>(a, pl, stream); break;
+            case 6: launch_mfma_k<D, 6, 2>(a, pl, stream); break;
+            case 7: launch_mfma_k<D, 7, 2>(a, pl, stream); break;
+            default: launch_mfma_k<D, 8, 2>(a, pl, stream); break;
+        }
+    }
+}
+
+template <typename T, int D>
+void launch_combine(const AttnArgs& a, int total_q, hipStream_t stream) {
     const int64_t items = (int64_t)total_q * a.hq;
     if (items > 0) {
         dim3 cgrid((unsigned)((items + kAttnWaves - 1) / kAttnWaves));
         hipLaunchKernelGGL((attn_combine<T, D>), cgrid, dim3(kAttnThreads), 0, stream, a, total_q);
     }
+}
+
+template <typename T, int D>
+void launch(const AttnArgs& a, const AttnPlan& pl, int total_q, hipStream_t stream) {
+    if constexpr (sizeof(T) == 2) {
+        launch_mfma<D>(a, pl, stream);
+    } else {
+        dim3 grid(pl.max_splits, a.hkv * pl.row_groups, a.num_seqs);
+        hipLaunchKernelGGL((attn_valu<T, D>), grid, dim3(kAttnThreads), 0, stream, a);
+    }
+    launch_combine<T, D>(a, total_q, stream);
 }
 
 }  // namespace
