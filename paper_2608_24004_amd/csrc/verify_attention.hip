@@ -16,7 +16,13 @@
 // Masks.  Row j of request i sits at position p = S_i - n_i + j and sees keys
 // t <= p, and with a sliding window W only t > p - W; the walk covers the
 // union of the rows' visible blocks only.
+#include <atomic>
+
 #include "common.h"
+
+// m0 is set inside the global->LDS load sequence (see dma16); the compiler
+// reloads m0 before each of its own uses, so clobbering it there is safe.
+#pragma clang diagnostic ignored "-Winline-asm"
 
 namespace averify {
 namespace {
@@ -227,121 +233,349 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
 
 // ------------------------------------------------------------------ MFMA path (bf16)
 //
-// Work item as for the VALU path, with up to NW*TPW*16 rows.  The workgroup's
-// NW wavefronts split the query rows (TPW tiles of 16 rows each) and share the
-// KV blocks: every block's K and V tiles (16 tokens x D, contiguous in the
-// paged layout) are loaded once per workgroup with 16-byte coalesced loads,
-// staged through a double-buffered LDS ring, and read by every wavefront as
-// MFMA operands.  Two blocks are in flight in registers while the current one
-// is consumed.
+// Persistent, load-balanced schedule.  A unit is one 16-token KV block of one
+// (request i, KV head g, row group) pair; units are numbered request by
+// request, then head, then row group, then block.  attn_schedule writes the
+// per-request unit offsets (a prefix sum over the batch), then attn_persist
+// launches a fixed number of workgroups (all resident at once) and gives
+// workgroup w the contiguous unit range [U*w/N, U*(w+1)/N), N = min(NWG, U): every
+// workgroup streams the same number of KV bytes whatever the context lengths,
+// so no workgroup is left running alone at the end.  A pair whose units all
+// fall in one range is finished in place; a pair cut by a range boundary
+// leaves one partial (normalised output + log-sum-exp) per workgroup in slot
+// P + w (P = pair index), and attn_combine_slots merges them.
+//
+// Inside a workgroup the NW wavefronts split the pair's query rows (TPW tiles
+// of 16 rows each) and share the KV blocks: each block's K and V tiles (16
+// tokens x D, contiguous in the paged layout) are loaded once with 16-byte
+// coalesced loads, PD blocks ahead, into registers, written to a
+// double-buffered LDS ring and read by every wavefront as MFMA operands.
+// The load stream runs straight across pair boundaries.
 //
 // Per block and 16-row tile, with lane = 16*lg + l16:
 //   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K (16 keys x 32 dims, lane
 //                 holds 8 consecutive dims of key l16: one 16-byte LDS read
 //                 of the x-packed K tile), B = Q^T (8 dims of row l16);
-//                 result lane holds keys 4lg..4lg+3 of row l16;
-//   O^T += V^T P^T v_mfma_f32_16x16x16_bf16, A = V^T (dims x 16 keys, lane
+//                 the result lane holds keys 4lg..4lg+3 of row l16;
+//   O^T += V^T P^T v_mfma_f32_16x16x16_bf16, A = V^T (16 dims x 16 keys, lane
 //                 holds 4 keys of dim l16: one 8-byte read of the V^T tile),
 //                 B = P^T (the same 4 keys of row l16, straight from the S
 //                 registers after the online-softmax update).
 // The output tile is O^T: lane holds dims 4lg..4lg+3 of row l16, so a row's
-// state (running max, rescale factor) lives in the lanes that own its scores.
+// running max and rescale factor live in the lanes that own its scores.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+// s_waitcnt immediate (gfx9 encoding) that waits for vmcnt == 0 and leaves
+// expcnt (bits 6:4) and lgkmcnt (bits 11:8) at their no-wait maxima.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Workgroup barrier that orders LDS only: the KV ring lives in LDS and global
+// memory needs no ordering between the waves of a workgroup here.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// 16 bytes per lane from global memory straight into LDS (gfx950
+// global_load_lds_dwordx4): lane l of the wavefront writes LDS bytes
+// [lds + 16 l, lds + 16 l + 16).  The load is issued from inline assembly so
+// that its completion is tracked by the explicit waits of the KV pipeline
+// alone; the compiler does not see it and adds no waits of its own.
+__device__ __forceinline__ void dma16(uint32_t lds_wave_base, const void* src) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_wave_base)), "v"(src)
+                 : "memory", "m0");
+}
+
+// Wait until at most N vector-memory operations of this wavefront are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+
+// Scalars of the persistent launch.  The pointers travel as separate
+// __restrict__ kernel arguments (MPtrs) so that the compiler can prove the
+// metadata arrays are never written by the kernel and read them with scalar
+// loads: a vector load there would make every wait on it drain the KV
+// prefetch queue.
+struct PArgs {
+    int num_seqs, hq, hkv, group, max_blocks, num_blocks, window, max_seq_len;
+    float scale_log2;
+    int rows_per_group;   // NW * TPW * 16
+    int rg_max;           // row groups per (request, KV head) at most
+    int nwg;              // workgroups of the persistent launch
+    int spb;              // > 0: fixed number of units per workgroup
+};
+
+struct MPtrs {
+    const uint16_t* q;
+    const uint8_t* kc;
+    const uint8_t* vc;
+    const int32_t* block_tables;
+    const int32_t* seq_lens;
+    const int32_t* q_start;
+    uint16_t* out;
+    int32_t* unit_start;  // [num_seqs + 1] first unit of each request (schedule pass)
+    float* slot_o;        // [slots][rows_per_group][D] normalised partial outputs
+    float* slot_lse;      // [slots][rows_per_group]    their log2-sum-exp
+};
+
+struct ReqGeom {
+    int q0, n, S, b_lo, nb, rg;
+};
+
+__device__ __forceinline__ ReqGeom req_geom(const PArgs& a, const int32_t* __restrict__ q_start,
+                                            const int32_t* __restrict__ seq_lens, int i) {
+    ReqGeom r;
+    r.q0 = q_start[i];
+    r.n = q_start[i + 1] - r.q0;
+    int S = seq_lens[i];
+    S = max(0, min(S, min(a.max_seq_len, a.max_blocks * kBlockTokens)));
+    r.S = S;
+    const int key_lo = a.window > 0 ? max(0, S - r.n - a.window + 1) : 0;
+    r.b_lo = key_lo / kBlockTokens;
+    const int b_hi = (S + kBlockTokens - 1) / kBlockTokens;
+    r.nb = max(0, b_hi - r.b_lo);
+    const int rows = a.group * max(0, r.n);
+    r.rg = min(a.rg_max, (rows + a.rows_per_group - 1) / a.rows_per_group);
+    return r;
 }
 
-template <int D, int NW, int TPW>
-__global__ __launch_bounds__(NW * kWave) void attn_mfma(AttnArgs a) {
+// Workgroups that share the U units in equal-share mode: at most one per unit,
+// so that every participating workgroup owns at least one unit.
+__device__ __forceinline__ int sharing_wgs(const PArgs& a, int U) { return min(a.nwg, max(U, 1)); }
+
+// Workgroup that owns unit u (inverse of the range split).
+__device__ __forceinline__ int owner_of(const PArgs& a, int u, int U) {
+    if (a.spb > 0) return u / a.spb;
+    return (int)(((int64_t)(u + 1) * sharing_wgs(a, U) - 1) / U);
+}
+
+// One workgroup: exclusive prefix sum of Hkv * row_groups * blocks over the batch.
+__global__ __launch_bounds__(1024) void attn_schedule(PArgs a, const int32_t* __restrict__ q_start,
+                                                     const int32_t* __restrict__ seq_lens,
+                                                     int32_t* __restrict__ unit_start) {
+    __shared__ int wsum[16];
+    __shared__ int carry_s;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+    if (tid == 0) carry_s = 0;
+    __syncthreads();
+    for (int base = 0; base < a.num_seqs; base += 1024) {
+        const int i = base + tid;
+        int u = 0;
+        if (i < a.num_seqs) {
+            const ReqGeom r = req_geom(a, q_start, seq_lens, i);
+            u = a.hkv * r.rg * r.nb;
+        }
+        int x = u;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        if (lane == kWave - 1) wsum[wv] = x;
+        __syncthreads();
+        if (wv == 0) {
+            int sv = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) {
+                const int y = __shfl_up(sv, o);
+                if (lane >= o) sv += y;
+            }
+            if (lane < 16) wsum[lane] = sv;
+        }
+        __syncthreads();
+        const int excl = carry_s + (wv > 0 ? wsum[wv - 1] : 0) + x - u;
+        if (i < a.num_seqs) unit_start[i] = excl;
+        __syncthreads();
+        if (tid == 1023) carry_s = excl + u;
+        __syncthreads();
+    }
+    if (tid == 0) unit_start[a.num_seqs] = carry_s;
+}
+
+struct Cursor {
+    int i, pq, b;  // request, pair within the request (head * rg + row group), block
+    ReqGeom rq;
+};
+
+__device__ __forceinline__ void advance(const PArgs& a, const int32_t* __restrict__ q_start,
+                                        const int32_t* __restrict__ seq_lens, Cursor& c) {
+    if (++c.b < c.rq.b_lo + c.rq.nb) return;
+    c.b = c.rq.b_lo;
+    if (++c.pq < a.hkv * c.rq.rg) return;
+    c.pq = 0;
+    while (++c.i < a.num_seqs) {
+        c.rq = req_geom(a, q_start, seq_lens, c.i);
+        if (c.rq.rg > 0 && c.rq.nb > 0) break;
+    }
+    c.b = c.rq.b_lo;
+}
+
+template <int D, int NW, int TPW, int PD>
+__global__ __launch_bounds__(NW * kWave) void attn_persist(
+    PArgs a, const uint16_t* __restrict__ qg, const uint8_t* __restrict__ kcg,
+    const uint8_t* __restrict__ vcg, const int32_t* __restrict__ block_tables,
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
+    const int32_t* __restrict__ unit_start, uint16_t* __restrict__ out,
+    float* __restrict__ slot_o, float* __restrict__ slot_lse) {
     constexpr int NT = NW * kWave;
     constexpr int TILE_BYTES = kBlockTokens * D * 2;  // one (block, head) K or V tile
     constexpr int CH = 2 * TILE_BYTES / 16;           // 16-byte chunks per block (K then V)
-    constexpr int CPT = (CH + NT - 1) / NT;           // chunks per thread per block
+    constexpr int CPT = CH / NT;                      // chunks per thread per block
     constexpr int KC = D / 32;                        // QK^T steps of 32 dims
     constexpr int DT = D / 16;                        // PV output tiles of 16 dims
     constexpr int ROWS = NW * TPW * 16;
+    constexpr int NS = PD + 1;                        // LDS stages: PD blocks in flight
+    static_assert(CH % NT == 0, "every thread loads the same number of chunks");
+    static_assert(CPT * (NS - 2) < 64, "vmcnt range");
 
-    __shared__ __attribute__((aligned(16))) uint8_t stage[2][2 * TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) uint8_t stage[NS][2 * TILE_BYTES];
 
-    const int i = blockIdx.z;
-    const int kvh = blockIdx.y / a.row_groups;
-    const int rg = blockIdx.y - kvh * a.row_groups;
-    const int s = blockIdx.x;
-    const SeqGeom sg = seq_geom(a, i);
-    const int rows_total = a.group * sg.n;
-    const int r0 = rg * ROWS;
-    if (r0 >= rows_total || s >= sg.nsplit) return;
-    const int sb = sg.b_lo + s * a.split_blocks;
-    const int se = min(sg.b_hi, sb + a.split_blocks);
+    const int w = blockIdx.x;
+    const int U = unit_start[a.num_seqs];
+    int us, ue;
+    if (a.spb > 0) {
+        us = (int)min((int64_t)U, (int64_t)w * a.spb);
+        ue = (int)min((int64_t)U, (int64_t)us + a.spb);
+    } else {
+        const int n = sharing_wgs(a, U);
+        if (w >= n) return;
+        us = (int)((int64_t)U * w / n);
+        ue = (int)((int64_t)U * (w + 1) / n);
+    }
+    if (us >= ue) return;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int w = tid / kWave;
+    const int wv = tid / kWave;
     const int l16 = lane & 15, lg = lane >> 4;
-    const int wrow0 = r0 + w * TPW * 16;          // first row of this wavefront
-    const bool active = wrow0 < rows_total;       // wavefront-uniform
 
-    // Q operands of this lane's rows (zeros for padding rows)
+    // request owning the first unit: the largest i with unit_start[i] <= us
+    Cursor c0;
+    {
+        int lo = 0, hi = a.num_seqs - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (unit_start[mid] <= us) lo = mid; else hi = mid - 1;
+        }
+        c0.i = lo;
+        c0.rq = req_geom(a, q_start, seq_lens, lo);
+        const int off = us - unit_start[lo];
+        c0.pq = off / c0.rq.nb;
+        c0.b = c0.rq.b_lo + (off - c0.pq * c0.rq.nb);
+    }
+
+    // One unit = one block's K and V tiles, copied into an LDS stage with CPT
+    // global->LDS loads per thread (wavefront w's c-th load fills the 1 KiB
+    // at chunk c*NT + 64w).  Every call issues exactly CPT loads, invalid
+    // block ids reading block 0 (compute skips them), so the explicit vmcnt
+    // waits below count exactly.
+    const uint32_t stage_lds =
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)&stage[0][0];
+    auto dma_unit = [&](const Cursor& c, int st) {
+        const int g = c.rq.rg == 1 ? c.pq : c.pq / c.rq.rg;
+        int phys = block_tables[(int64_t)c.i * a.max_blocks + c.b];
+        phys = (phys < 0 || phys >= a.num_blocks) ? 0 : phys;
+        const int64_t off = ((int64_t)phys * a.hkv + g) * TILE_BYTES;
+        const uint32_t base = stage_lds + st * (2 * TILE_BYTES);
+#pragma unroll
+        for (int c2 = 0; c2 < CPT; ++c2) {
+            const int wchunk = c2 * NT + wv * kWave;  // first chunk of this wavefront's load
+            const int idx = wchunk + lane;
+            const uint8_t* srcp = idx < CH / 2 ? kcg + off + idx * 16 : vcg + off + (idx - CH / 2) * 16;
+            dma16(base + wchunk * 16, srcp);
+        }
+    };
+
+    // ---- state of the pair being computed
+    int st_i = -1, st_pq = -1, st_g = 0, st_rg = 0;
+    ReqGeom srq{};
+    bool active = false;
     bf16x8_t qop[TPW][KC];
     int row_j[TPW];
-    const uint16_t* qp = static_cast<const uint16_t*>(a.q);
-#pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-        const int rr = wrow0 + t * 16 + l16;
-        const bool valid = rr < rows_total;
-        const int j = rr / a.group, gh = rr - j * a.group;
-        row_j[t] = valid ? j : -1;
-        const int64_t base = ((int64_t)(sg.q0 + j) * a.hq + kvh * a.group + gh) * D;
-#pragma unroll
-        for (int cc = 0; cc < KC; ++cc) {
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (valid) v = ld16(qp + base + (cc * 4 + lg) * 8);
-            qop[t][cc] = as_bf16x8(v);
-        }
-    }
-
     f32x4_t o[TPW][DT];
     float m_r[TPW], l_r[TPW];
-#pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-        m_r[t] = -INFINITY;
-        l_r[t] = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
 
-    const uint8_t* kbase = static_cast<const uint8_t*>(a.kc);
-    const uint8_t* vbase = static_cast<const uint8_t*>(a.vc);
-    const int32_t* btab = a.block_tables + (int64_t)i * a.max_blocks;
-    const int p_first = sg.S - sg.n;   // position of the request's first query row
-
-    auto load_block = [&](int b, uint4* regs) {
-        const int phys = btab[b];
-        if (phys < 0 || phys >= a.num_blocks) return;
-        const int64_t off = ((int64_t)phys * a.hkv + kvh) * TILE_BYTES;
+    auto init_pair = [&](const Cursor& c) {
+        st_i = c.i;
+        st_pq = c.pq;
+        srq = c.rq;
+        st_g = c.pq / c.rq.rg;
+        st_rg = c.pq - st_g * c.rq.rg;
+        const int rows = a.group * srq.n;
+        const int wrow0 = st_rg * ROWS + wv * TPW * 16;
+        active = wrow0 < rows;
 #pragma unroll
-        for (int c = 0; c < CPT; ++c) {
-            const int idx = tid + c * NT;
-            if (CH % NT == 0 || idx < CH) {
-                const uint8_t* src = idx < CH / 2 ? kbase + off + idx * 16 : vbase + off + (idx - CH / 2) * 16;
-                regs[c] = ld16(src);
+        for (int t = 0; t < TPW; ++t) {
+            const int rr = wrow0 + t * 16 + l16;
+            const bool valid = rr < rows;
+            const int j = rr / a.group, gh = rr - j * a.group;
+            row_j[t] = valid ? j : -1;
+            const int64_t base = ((int64_t)(srq.q0 + j) * a.hq + st_g * a.group + gh) * D;
+#pragma unroll
+            for (int cc = 0; cc < KC; ++cc) {
+                uint4 v = make_uint4(0, 0, 0, 0);
+                if (valid) v = ld16(qg + base + (cc * 4 + lg) * 8);
+                qop[t][cc] = as_bf16x8(v);
+            }
+            m_r[t] = -INFINITY;
+            l_r[t] = 0.f;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+        // Settle the Q loads here, on the (rare) pair-switch path.  Otherwise
+        // the compiler cannot tell whether they are still in flight when the
+        // next block's MFMA reads the operands, and waits for the whole load
+        // queue, prefetched KV blocks included, before every block.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    };
+
+    auto flush_pair = [&]() {
+        if (!active) return;
+        const int ps = unit_start[st_i] + st_pq * srq.nb;
+        const bool whole = ps >= us && ps + srq.nb <= ue;
+        const int rows = a.group * srq.n;
+        const int64_t slot = (int64_t)(st_i * a.hkv + st_g) * a.rg_max + st_rg + w;
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            float L = l_r[t];
+            L += __shfl_xor(L, 16);
+            L += __shfl_xor(L, 32);
+            const int lr = (wv * TPW + t) * 16 + l16;
+            const int rr = st_rg * ROWS + lr;
+            if (rr >= rows) continue;
+            const float inv = L > 0.f ? 1.f / L : 0.f;
+            if (whole) {
+                const int j = rr / a.group, gh = rr - j * a.group;
+                const int64_t hrow = (int64_t)(srq.q0 + j) * a.hq + st_g * a.group + gh;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const int d0 = dt * 16 + 4 * lg;
+                    const uint2 v = make_uint2(pack_bf16x2(o[t][dt][0] * inv, o[t][dt][1] * inv),
+                                               pack_bf16x2(o[t][dt][2] * inv, o[t][dt][3] * inv));
+                    *reinterpret_cast<uint2*>(out + hrow * D + d0) = v;
+                }
+            } else {
+                const int64_t srow = slot * ROWS + lr;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+                    *reinterpret_cast<f32x4_t*>(slot_o + srow * D + dt * 16 + 4 * lg) = o[t][dt] * inv;
+                if (lg == 0) slot_lse[srow] = L > 0.f ? m_r[t] + log2f(L) : -INFINITY;
             }
         }
     };
-    auto store_block = [&](int st, const uint4* regs) {
-#pragma unroll
-        for (int c = 0; c < CPT; ++c) {
-            const int idx = tid + c * NT;
-            if (CH % NT == 0 || idx < CH) *reinterpret_cast<uint4*>(&stage[st][idx * 16]) = regs[c];
-        }
-    };
+
     auto compute = [&](int st, int b) {
-        const int phys = btab[b];
+        const int phys = block_tables[(int64_t)st_i * a.max_blocks + b];
         if (!active || phys < 0 || phys >= a.num_blocks) return;
         const uint8_t* ks = stage[st];
         const uint8_t* vs = stage[st] + TILE_BYTES;
@@ -350,16 +584,18 @@ __global__ __launch_bounds__(NW * kWave) void attn_mfma(AttnArgs a) {
         for (int t = 0; t < TPW; ++t) sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int cc = 0; cc < KC; ++cc) {
-            const bf16x8_t kop = as_bf16x8(*reinterpret_cast<const uint4*>(ks + ((cc * 4 + lg) * 16 + l16) * 16));
+            const bf16x8_t kop =
+                as_bf16x8(*reinterpret_cast<const uint4*>(ks + ((cc * 4 + lg) * 16 + l16) * 16));
 #pragma unroll
             for (int t = 0; t < TPW; ++t)
                 sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[t][cc], sacc[t], 0, 0, 0);
         }
+        const int p_first = srq.S - srq.n;  // position of the request's first query row
         const int key0 = b * kBlockTokens + 4 * lg;
-        // blocks entirely below the first row's position and inside the last
-        // row's window need no mask
+        // blocks below the first row's position and inside the last row's
+        // window are fully visible to every row of the request
         const bool need_mask = (b * kBlockTokens + kBlockTokens - 1 > p_first) ||
-                               (a.window > 0 && b * kBlockTokens < sg.S - a.window);
+                               (a.window > 0 && b * kBlockTokens < srq.S - a.window);
         i16x4_t pop[TPW];
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
@@ -380,16 +616,24 @@ __global__ __launch_bounds__(NW * kWave) void attn_mfma(AttnArgs a) {
             mx = fmaxf(mx, __shfl_xor(mx, 32));
             const float mnew = fmaxf(m_r[t], mx);
             const float muse = mnew == -INFINITY ? 0.f : mnew;
-            const float alpha = exp2f(m_r[t] - muse);
+            // exponent arguments are <= 0: the raw v_exp_f32 is exact enough
+            // and results below 2^-126 only flush to zero
+            const float alpha = __builtin_amdgcn_exp2f(m_r[t] - muse);
             float pr[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) pr[r] = exp2f(sv[r] - muse);
+            for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(sv[r] - muse);
             l_r[t] = l_r[t] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
+            // The accumulated output only needs rescaling when a row's running
+            // maximum grew (and it already held something); after the first
+            // blocks that is rare, so test it once for the whole wavefront.
+            const bool grew = alpha != 1.f && m_r[t] != -INFINITY;
             m_r[t] = mnew;
-            const uint32_t lo = pack_bf16x2(pr[0], pr[1]), hi = pack_bf16x2(pr[2], pr[3]);
-            pop[t] = __builtin_bit_cast(i16x4_t, make_uint2(lo, hi));
+            pop[t] = __builtin_bit_cast(i16x4_t, make_uint2(pack_bf16x2(pr[0], pr[1]),
+                                                            pack_bf16x2(pr[2], pr[3])));
+            if (__builtin_amdgcn_ballot_w64(grew)) {
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
+                for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
+            }
         }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
@@ -401,55 +645,102 @@ __global__ __launch_bounds__(NW * kWave) void attn_mfma(AttnArgs a) {
         }
     };
 
-    // double-buffered LDS ring fed by two register sets
-    uint4 pa[CPT], pb[CPT];
-    if (sb < se) load_block(sb, pa);
-    if (sb + 1 < se) load_block(sb + 1, pb);
-    if (sb < se) store_block(0, pa);
-    if (sb + 2 < se) load_block(sb + 2, pa);
-    __syncthreads();
-    for (int b = sb; b < se; b += 2) {
-        compute(0, b);
-        if (b + 1 < se) store_block(1, pb);
-        if (b + 3 < se) load_block(b + 3, pb);
-        __syncthreads();
-        if (b + 1 >= se) break;
-        compute(1, b + 1);
-        if (b + 2 < se) store_block(0, pa);
-        if (b + 4 < se) load_block(b + 4, pa);
-        __syncthreads();
-    }
+    // ---- pipeline: a ring of NS = PD + 1 LDS stages, PD blocks in flight.
+    // At unit uu: wait for this thread's loads of uu (the PD - 1 younger units
+    // may stay in flight), barrier (everyone's loads of uu have landed and
+    // everyone is done with uu - 1), refill the stage of uu - 1 with unit
+    // uu + PD, compute uu.  The loader cursor stops at the last unit and loads
+    // it again instead of issuing nothing, keeping the count fixed.
+    Cursor lc = c0;
+    int lu = us;
+    auto dma_next = [&](int st) {
+        dma_unit(lc, st);
+        if (lu + 1 < ue) {
+            advance(a, q_start, seq_lens, lc);
+            ++lu;
+        }
+    };
+#pragma unroll
+    for (int r = 0; r < PD; ++r) dma_next(r);
 
-    if (!active) return;
-    uint16_t* outp = static_cast<uint16_t*>(a.out);
-#pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-        float L = l_r[t];
-        L += __shfl_xor(L, 16);
-        L += __shfl_xor(L, 32);
-        const int rr = wrow0 + t * 16 + l16;
-        if (rr >= rows_total) continue;
-        const int j = rr / a.group, gh = rr - j * a.group;
-        const int64_t hrow = (int64_t)(sg.q0 + j) * a.hq + kvh * a.group + gh;
-        const float inv = L > 0.f ? 1.f / L : 0.f;
-        if (sg.nsplit == 1) {
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const int d0 = dt * 16 + 4 * lg;
-                const uint2 v = make_uint2(pack_bf16x2(o[t][dt][0] * inv, o[t][dt][1] * inv),
-                                           pack_bf16x2(o[t][dt][2] * inv, o[t][dt][3] * inv));
-                *reinterpret_cast<uint2*>(outp + hrow * D + d0) = v;
+    Cursor cc = c0;
+    init_pair(cc);
+    int st = 0;
+    for (int uu = us; uu < ue; ++uu) {
+        wait_vmcnt<CPT * (PD - 1)>();
+        lds_barrier();
+        dma_next(st == 0 ? NS - 1 : st - 1);
+        if (cc.i != st_i || cc.pq != st_pq) {
+            flush_pair();
+            init_pair(cc);
+        }
+        compute(st, cc.b);
+        advance(a, q_start, seq_lens, cc);
+        st = st == NS - 1 ? 0 : st + 1;
+    }
+    // no global->LDS load may still be writing when the workgroup's LDS is freed
+    wait_vmcnt<0>();
+    flush_pair();
+}
+
+// Merges the partial slots of pairs cut by workgroup range boundaries, and
+// writes the zero output of rows whose request has no key.  Grid (pairs, row
+// chunks); a thread owns one row and four consecutive output dimensions, so
+// all of a thread's slot reads are independent and issued together.
+constexpr int kCombineThreads = 256;
+
+template <int D>
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
+    PArgs a, const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
+    const int32_t* __restrict__ unit_start, const float* __restrict__ slot_o,
+    const float* __restrict__ slot_lse, uint16_t* __restrict__ out) {
+    constexpr int QUADS = D / 4;                       // 4-dim vectors per row
+    constexpr int RPB = kCombineThreads / QUADS;       // rows per workgroup
+    const int P = blockIdx.x;
+    const int per_req = a.hkv * a.rg_max;
+    const int i = P / per_req;
+    const int rem = P - i * per_req;
+    const int g = rem / a.rg_max, rg = rem - g * a.rg_max;
+    const ReqGeom rq = req_geom(a, q_start, seq_lens, i);
+    if (rg >= rq.rg) return;
+    const int ROWS = a.rows_per_group;
+    const int rows = a.group * rq.n;
+    const int lr = blockIdx.y * RPB + threadIdx.x / QUADS;  // row within the group
+    const int rr = rg * ROWS + lr;
+    if (lr >= ROWS || rr >= rows) return;
+    const bool empty = rq.nb == 0;
+    int wf = 0, wl = 0;
+    if (!empty) {
+        const int U = unit_start[a.num_seqs];
+        const int ps = unit_start[i] + (g * rq.rg + rg) * rq.nb;
+        wf = owner_of(a, ps, U);
+        wl = owner_of(a, ps + rq.nb - 1, U);
+        if (wf == wl) return;  // finished in place by its only workgroup
+    }
+    const int d0 = (threadIdx.x % QUADS) * 4;
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    if (!empty) {
+        const int64_t slot0 = (int64_t)P + wf;
+        const int ns = wl - wf + 1;
+        float M = -INFINITY;
+        for (int s = 0; s < ns; ++s) M = fmaxf(M, slot_lse[(slot0 + s) * ROWS + lr]);
+        if (M != -INFINITY) {
+            float L = 0.f;
+            for (int s = 0; s < ns; ++s) {
+                const int64_t srow = (slot0 + s) * ROWS + lr;
+                const float lse = slot_lse[srow];
+                const f32x4_t o = *reinterpret_cast<const f32x4_t*>(slot_o + srow * D + d0);
+                const float f = lse == -INFINITY ? 0.f : exp2f(lse - M);
+                L += f;
+                acc += f * o;
             }
-        } else {
-            const int64_t pi = hrow * a.max_splits + s;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const int d0 = dt * 16 + 4 * lg;
-                *reinterpret_cast<f32x4_t*>(a.part_o + pi * D + d0) = o[t][dt] * inv;
-            }
-            if (lg == 0) a.part_lse[pi] = L > 0.f ? m_r[t] + log2f(L) : -INFINITY;
+            acc *= 1.f / L;
         }
     }
+    const int j = rr / a.group, gh = rr - j * a.group;
+    const int64_t hrow = (int64_t)(rq.q0 + j) * a.hq + g * a.group + gh;
+    *reinterpret_cast<uint2*>(out + hrow * D + d0) =
+        make_uint2(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]));
 }
 
 // ------------------------------------------------------------------ combine
@@ -501,14 +792,26 @@ __global__ __launch_bounds__(kAttnThreads) void attn_combine(AttnArgs a, int tot
 // ------------------------------------------------------------------ host side
 
 struct AttnPlan {
-    bool mfma;        // bf16 storage: MFMA kernel; fp32 storage: VALU kernel
-    int nw, tpw;      // MFMA: wavefronts per workgroup, 16-row tiles per wavefront
+    bool mfma;        // bf16 storage: persistent MFMA kernel; fp32 storage: VALU kernel
+    // VALU path
     int split_blocks;
     int max_splits;
     int row_groups;
     size_t part_o_bytes;
     size_t part_lse_bytes;
+    // MFMA path
+    int nw, tpw;      // wavefronts per workgroup, 16-row tiles per wavefront
+    int rg_max;       // row groups per (request, KV head)
+    int nwg;          // persistent workgroups
+    int spb;          // fixed units per workgroup (0: equal shares)
+    int64_t slots;    // partial slots
+    size_t unit_bytes, slot_o_bytes, slot_lse_bytes;
+    size_t total_bytes;
 };
+
+// KV blocks in flight per workgroup: single-wavefront workers keep three
+// (24 KiB at D = 128) so that five fit a compute unit's LDS.
+constexpr int prefetch_depth(int nw) { return nw == 1 ? 3 : 4; }
 
 int validate(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
              int32_t max_seq_len) {
@@ -525,8 +828,80 @@ int validate(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
     return VERIFY_OK;
 }
 
-AttnPlan make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
-                   int32_t max_seq_len) {
+// Compute units of the current device and resident workgroups per compute
+// unit of a kernel (cached per device; fallbacks when no device is visible).
+int device_cus() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 256; }
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) {
+        (void)hipGetLastError();
+        v = 256;
+    }
+    cache[dev].store(v, std::memory_order_relaxed);
+    return v;
+}
+
+template <int D, int NW, int TPW>
+int resident_wgs() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 2; }
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, attn_persist<D, NW, TPW, prefetch_depth(NW)>,
+                                                     NW * kWave, 0) != hipSuccess || v <= 0) {
+        (void)hipGetLastError();
+        v = 1;
+    }
+    cache[dev].store(v, std::memory_order_relaxed);
+    return v;
+}
+
+template <int D>
+int resident_wgs_for(int nw, int tpw) {
+    if (nw == 1) {
+        switch (tpw) {
+            case 1: return resident_wgs<D, 1, 1>();
+            case 2: return resident_wgs<D, 1, 2>();
+            case 3: return resident_wgs<D, 1, 3>();
+            case 4: return resident_wgs<D, 1, 4>();
+        }
+        if constexpr (D == 64) {
+            switch (tpw) {
+                case 5: return resident_wgs<D, 1, 5>();
+                case 6: return resident_wgs<D, 1, 6>();
+                default: return resident_wgs<D, 1, 8>();
+            }
+        }
+        return 1;
+    }
+    if constexpr (D == 128) {
+        if (nw == 2) return tpw == 1 ? resident_wgs<D, 2, 1>() : resident_wgs<D, 2, 2>();
+        if (nw == 4) return tpw == 1 ? resident_wgs<D, 4, 1>() : resident_wgs<D, 4, 2>();
+        return tpw == 1 ? resident_wgs<D, 8, 1>() : resident_wgs<D, 8, 2>();
+    } else {
+        if (nw == 2) {
+            switch (tpw) {
+                case 1: return resident_wgs<D, 2, 1>();
+                case 2: return resident_wgs<D, 2, 2>();
+                case 3: return resident_wgs<D, 2, 3>();
+                default: return resident_wgs<D, 2, 4>();
+            }
+        }
+        switch (tpw) {
+            case 1: return resident_wgs<D, 4, 1>();
+            case 2: return resident_wgs<D, 4, 2>();
+            case 3: return resident_wgs<D, 4, 3>();
+            default: return resident_wgs<D, 4, 4>();
+        }
+    }
+}
+
+int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
+              int32_t max_seq_len, AttnPlan* out) {
     AttnPlan pl{};
     const int G = p->num_q_heads / p->num_kv_heads;
     int64_t nb_max = ((int64_t)max_seq_len + kBlockTokens - 1) / kBlockTokens;
@@ -535,82 +910,138 @@ AttnPlan make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_l
         nb_max = std::min<int64_t>(nb_max, (span + kBlockTokens - 1) / kBlockTokens + 1);
     }
     nb_max = std::max<int64_t>(nb_max, 1);
-    int sb = p->kv_split_blocks;
-    if (sb == 0) {
-        // aim for about 8192 work items over the batch, at least 32 blocks per split
-        const int64_t total = (int64_t)std::max(1, p->num_seqs) * p->num_kv_heads * nb_max;
-        int64_t want = (total + 8191) / 8192;
-        want = std::max<int64_t>(32, (want + 3) / 4 * 4);
-        sb = (int)std::min<int64_t>(want, nb_max);
-    }
-    pl.split_blocks = std::max(1, sb);
-    pl.max_splits = (int)((nb_max + pl.split_blocks - 1) / pl.split_blocks);
     const int64_t rows = (int64_t)G * std::max(1, max_q_len);
     pl.mfma = p->dtype == VERIFY_BF16;
     if (pl.mfma) {
+        // A single tile goes to single-wavefront workgroups: every wavefront is
+        // an independent worker with its own LDS ring and no barrier.  More
+        // rows use NW wavefronts sharing one ring, one or two tiles each (a
+        // wavefront holding all tiles runs at one wave per SIMD and cannot hide
+        // its latencies); NW divides the 16-byte chunks of a block (512 at
+        // D = 128, 256 at D = 64) so every thread loads alike.
         const int64_t tiles = (rows + 15) / 16;
-        if (tiles <= 8) { pl.tpw = 1; pl.nw = (int)std::max<int64_t>(2, tiles); }
-        else if (tiles <= 16) { pl.tpw = 2; pl.nw = (int)((tiles + 1) / 2); }
-        else { pl.tpw = 2; pl.nw = 8; }
+        const int tpw1_max = 1;
+        if (tiles <= tpw1_max) {
+            pl.nw = 1;
+            pl.tpw = (int)tiles;
+            if (p->head_dim == 64 && pl.tpw == 7) pl.tpw = 8;
+        } else {
+            const int nw_max = p->head_dim == 128 ? 8 : 4;
+            const int tpw_max = p->head_dim == 128 ? 2 : 4;
+            pl.nw = 2;
+            while (pl.nw < nw_max && pl.nw < tiles) pl.nw *= 2;
+            pl.tpw = (int)std::min<int64_t>(tpw_max, (tiles + pl.nw - 1) / pl.nw);
+        }
         const int64_t per = (int64_t)pl.nw * pl.tpw * 16;
-        pl.row_groups = (int)((rows + per - 1) / per);
+        pl.rg_max = (int)((rows + per - 1) / per);
+        const int64_t pairs = (int64_t)std::max(1, p->num_seqs) * p->num_kv_heads * pl.rg_max;
+        const int64_t units_max = pairs * nb_max;
+        if (units_max >= (int64_t)1 << 31) return VERIFY_EUNSUPPORTED;
+        pl.spb = p->kv_split_blocks;
+        if (pl.spb > 0) {
+            pl.nwg = (int)std::min<int64_t>((units_max + pl.spb - 1) / pl.spb, (int64_t)1 << 30);
+        } else {
+            const int res = p->head_dim == 128 ? resident_wgs_for<128>(pl.nw, pl.tpw)
+                                               : resident_wgs_for<64>(pl.nw, pl.tpw);
+            pl.nwg = device_cus() * res;
+        }
+        pl.slots = pairs + pl.nwg;
+        pl.unit_bytes = align_up(sizeof(int32_t) * ((size_t)std::max(1, p->num_seqs) + 1), 256);
+        pl.slot_o_bytes = align_up((size_t)pl.slots * per * p->head_dim * sizeof(float), 256);
+        pl.slot_lse_bytes = align_up((size_t)pl.slots * per * sizeof(float), 256);
+        pl.total_bytes = pl.unit_bytes + pl.slot_o_bytes + pl.slot_lse_bytes;
     } else {
+        int sb = p->kv_split_blocks;
+        if (sb == 0) {
+            // aim for about 8192 work items over the batch, at least 32 blocks per split
+            const int64_t total = (int64_t)std::max(1, p->num_seqs) * p->num_kv_heads * nb_max;
+            int64_t want = (total + 8191) / 8192;
+            want = std::max<int64_t>(32, (want + 3) / 4 * 4);
+            sb = (int)std::min<int64_t>(want, nb_max);
+        }
+        pl.split_blocks = std::max(1, sb);
+        pl.max_splits = (int)((nb_max + pl.split_blocks - 1) / pl.split_blocks);
         pl.row_groups = (int)((rows + kValuRows - 1) / kValuRows);
+        if (pl.max_splits > 1) {
+            const size_t items = (size_t)total_q * p->num_q_heads * pl.max_splits;
+            pl.part_o_bytes = align_up(items * p->head_dim * sizeof(float), 256);
+            pl.part_lse_bytes = align_up(items * sizeof(float), 256);
+        }
+        pl.total_bytes = pl.part_o_bytes + pl.part_lse_bytes;
     }
-    if (pl.max_splits > 1) {
-        const size_t items = (size_t)total_q * p->num_q_heads * pl.max_splits;
-        pl.part_o_bytes = align_up(items * p->head_dim * sizeof(float), 256);
-        pl.part_lse_bytes = align_up(items * sizeof(float), 256);
-    }
-    return pl;
+    *out = pl;
+    return VERIFY_OK;
 }
 
 template <int D, int NW, int TPW>
-void launch_mfma_k(const AttnArgs& a, const AttnPlan& pl, hipStream_t stream) {
-    dim3 grid(pl.max_splits, a.hkv * pl.row_groups, a.num_seqs);
-    hipLaunchKernelGGL((attn_mfma<D, NW, TPW>), grid, dim3(NW * kWave), 0, stream, a);
+void launch_persist_k(const PArgs& a, const MPtrs& m, hipStream_t stream) {
+    hipLaunchKernelGGL((attn_persist<D, NW, TPW, prefetch_depth(NW)>), dim3(a.nwg), dim3(NW * kWave), 0,
+                       stream, a, m.q, m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start,
+                       m.unit_start, m.out, m.slot_o, m.slot_lse);
 }
 
 template <int D>
-void launch_mfma(const AttnArgs& a, const AttnPlan& pl, hipStream_t stream) {
-    if (pl.tpw == 1) {
-        switch (pl.nw) {
-            case 2: launch_mfma_k<D, 2, 1>(a, pl, stream); break;
-            case 3: launch_mfma_k<D, 3, 1>(a, pl, stream); break;
-            case 4: launch_mfma_k<D, 4, 1>(a, pl, stream); break;
-            case 5: launch_mfma_k<D, 5, 1>(a, pl, stream); break;
-            case 6: launch_mfma_k<D, 6, 1>(a, pl, stream); break;
-            case 7: launch_mfma_k<D, 7, 1>(a, pl, stream); break;
-            default: launch_mfma_k<D, 8, 1>(a, pl, stream); break;
+void launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, hipStream_t stream) {
+    hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
+                       m.unit_start);
+    if (pl.nw == 1) {
+        switch (pl.tpw) {
+            case 1: launch_persist_k<D, 1, 1>(a, m, stream); break;
+            case 2: launch_persist_k<D, 1, 2>(a, m, stream); break;
+            case 3: launch_persist_k<D, 1, 3>(a, m, stream); break;
+            case 4: launch_persist_k<D, 1, 4>(a, m, stream); break;
+            default:
+                if constexpr (D == 64) {
+                    if (pl.tpw == 5) launch_persist_k<D, 1, 5>(a, m, stream);
+                    else if (pl.tpw == 6) launch_persist_k<D, 1, 6>(a, m, stream);
+                    else launch_persist_k<D, 1, 8>(a, m, stream);
+                }
+                break;
+        }
+    } else if constexpr (D == 128) {
+        if (pl.nw == 2) {
+            if (pl.tpw == 1) launch_persist_k<D, 2, 1>(a, m, stream);
+            else launch_persist_k<D, 2, 2>(a, m, stream);
+        } else if (pl.nw == 4) {
+            if (pl.tpw == 1) launch_persist_k<D, 4, 1>(a, m, stream);
+            else launch_persist_k<D, 4, 2>(a, m, stream);
+        } else {
+            if (pl.tpw == 1) launch_persist_k<D, 8, 1>(a, m, stream);
+            else launch_persist_k<D, 8, 2>(a, m, stream);
         }
     } else {
-        switch (pl.nw) {
-            case 5: launch_mfma_k<D, 5, 2>(a, pl, stream); break;
-            case 6: launch_mfma_k<D, 6, 2>(a, pl, stream); break;
-            case 7: launch_mfma_k<D, 7, 2>(a, pl, stream); break;
-            default: launch_mfma_k<D, 8, 2>(a, pl, stream); break;
+        if (pl.nw == 2) {
+            switch (pl.tpw) {
+                case 1: launch_persist_k<D, 2, 1>(a, m, stream); break;
+                case 2: launch_persist_k<D, 2, 2>(a, m, stream); break;
+                case 3: launch_persist_k<D, 2, 3>(a, m, stream); break;
+                default: launch_persist_k<D, 2, 4>(a, m, stream); break;
+            }
+        } else {
+            switch (pl.tpw) {
+                case 1: launch_persist_k<D, 4, 1>(a, m, stream); break;
+                case 2: launch_persist_k<D, 4, 2>(a, m, stream); break;
+                case 3: launch_persist_k<D, 4, 3>(a, m, stream); break;
+                default: launch_persist_k<D, 4, 4>(a, m, stream); break;
+            }
         }
     }
+    const int64_t pairs = (int64_t)a.num_seqs * a.hkv * a.rg_max;
+    constexpr int rpb = kCombineThreads / (D / 4);
+    const int chunks = (a.rows_per_group + rpb - 1) / rpb;
+    hipLaunchKernelGGL((attn_combine_slots<D>), dim3((unsigned)pairs, chunks), dim3(kCombineThreads),
+                       0, stream, a, m.seq_lens, m.q_start, m.unit_start, m.slot_o, m.slot_lse, m.out);
 }
 
 template <typename T, int D>
-void launch_combine(const AttnArgs& a, int total_q, hipStream_t stream) {
+void launch_valu(const AttnArgs& a, const AttnPlan& pl, int total_q, hipStream_t stream) {
+    dim3 grid(pl.max_splits, a.hkv * pl.row_groups, a.num_seqs);
+    hipLaunchKernelGGL((attn_valu<T, D>), grid, dim3(kAttnThreads), 0, stream, a);
     const int64_t items = (int64_t)total_q * a.hq;
     if (items > 0) {
         dim3 cgrid((unsigned)((items + kAttnWaves - 1) / kAttnWaves));
         hipLaunchKernelGGL((attn_combine<T, D>), cgrid, dim3(kAttnThreads), 0, stream, a, total_q);
     }
-}
-
-template <typename T, int D>
-void launch(const AttnArgs& a, const AttnPlan& pl, int total_q, hipStream_t stream) {
-    if constexpr (sizeof(T) == 2) {
-        launch_mfma<D>(a, pl, stream);
-    } else {
-        dim3 grid(pl.max_splits, a.hkv * pl.row_groups, a.num_seqs);
-        hipLaunchKernelGGL((attn_valu<T, D>), grid, dim3(kAttnThreads), 0, stream, a);
-    }
-    launch_combine<T, D>(a, total_q, stream);
 }
 
 }  // namespace
@@ -622,10 +1053,12 @@ extern "C" int verify_attention_workspace_size(const verify_attn_params* params,
                                                int32_t max_q_len, int32_t max_seq_len,
                                                size_t* bytes) {
     if (!bytes) return VERIFY_EINVAL;
-    const int rc = validate(params, total_q, max_q_len, max_seq_len);
+    int rc = validate(params, total_q, max_q_len, max_seq_len);
     if (rc != VERIFY_OK) return rc;
-    const AttnPlan pl = make_plan(params, total_q, max_q_len, max_seq_len);
-    *bytes = pl.part_o_bytes + pl.part_lse_bytes;
+    AttnPlan pl;
+    rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl);
+    if (rc != VERIFY_OK) return rc;
+    *bytes = pl.total_bytes;
     return VERIFY_OK;
 }
 
@@ -635,16 +1068,52 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
                                 const int32_t* block_tables, const int32_t* seq_lens,
                                 const int32_t* q_start, void* out, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream) {
-    const int rc = validate(params, total_q, max_q_len, max_seq_len);
+    int rc = validate(params, total_q, max_q_len, max_seq_len);
     if (rc != VERIFY_OK) return rc;
     const verify_attn_params& p = *params;
     if (p.num_seqs > 0 && (!seq_lens || !q_start || !block_tables)) return VERIFY_EINVAL;
     if (total_q > 0 && (!q || !k_cache || !v_cache || !out)) return VERIFY_EINVAL;
-    const AttnPlan pl = make_plan(params, total_q, max_q_len, max_seq_len);
-    const size_t need = pl.part_o_bytes + pl.part_lse_bytes;
-    if (workspace_bytes < need || (need > 0 && !workspace)) return VERIFY_EWORKSPACE;
-    if ((int64_t)p.num_kv_heads * pl.row_groups > 65535) return VERIFY_EUNSUPPORTED;
+    // a query row sits at a position of its own request, so its cache holds
+    // at least one block
+    if (total_q > 0 && p.num_blocks < 1) return VERIFY_EINVAL;
+    AttnPlan pl;
+    rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl);
+    if (rc != VERIFY_OK) return rc;
+    if (workspace_bytes < pl.total_bytes || (pl.total_bytes > 0 && !workspace)) return VERIFY_EWORKSPACE;
     if (p.num_seqs == 0 || total_q == 0) return VERIFY_OK;
+    const float scale = p.scale > 0.f ? p.scale : 1.0f / sqrtf((float)p.head_dim);
+
+    if (pl.mfma) {
+        MPtrs m{};
+        m.q = static_cast<const uint16_t*>(q);
+        m.kc = static_cast<const uint8_t*>(k_cache);
+        m.vc = static_cast<const uint8_t*>(v_cache);
+        m.block_tables = block_tables;
+        m.seq_lens = seq_lens;
+        m.q_start = q_start;
+        m.out = static_cast<uint16_t*>(out);
+        char* ws = static_cast<char*>(workspace);
+        m.unit_start = reinterpret_cast<int32_t*>(ws);
+        m.slot_o = reinterpret_cast<float*>(ws + pl.unit_bytes);
+        m.slot_lse = reinterpret_cast<float*>(ws + pl.unit_bytes + pl.slot_o_bytes);
+        PArgs a{};
+        a.num_seqs = p.num_seqs;
+        a.hq = p.num_q_heads;
+        a.hkv = p.num_kv_heads;
+        a.group = p.num_q_heads / p.num_kv_heads;
+        a.max_blocks = p.max_blocks_per_seq;
+        a.num_blocks = p.num_blocks;
+        a.window = p.sliding_window;
+        a.max_seq_len = max_seq_len;
+        a.scale_log2 = scale * kLog2e;
+        a.rows_per_group = pl.nw * pl.tpw * 16;
+        a.rg_max = pl.rg_max;
+        a.nwg = pl.nwg;
+        a.spb = pl.spb;
+        if (p.head_dim == 128) launch_persist<128>(a, m, pl, stream);
+        else launch_persist<64>(a, m, pl, stream);
+        return check_launch();
+    }
 
     AttnArgs a{};
     a.q = q;
@@ -654,9 +1123,10 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
     a.seq_lens = seq_lens;
     a.q_start = q_start;
     a.out = out;
-    a.part_o = need ? static_cast<float*>(workspace) : nullptr;
-    a.part_lse = need ? reinterpret_cast<float*>(static_cast<char*>(workspace) + pl.part_o_bytes)
-                      : nullptr;
+    a.part_o = pl.part_o_bytes ? static_cast<float*>(workspace) : nullptr;
+    a.part_lse = pl.part_o_bytes
+                     ? reinterpret_cast<float*>(static_cast<char*>(workspace) + pl.part_o_bytes)
+                     : nullptr;
     a.num_seqs = p.num_seqs;
     a.hq = p.num_q_heads;
     a.hkv = p.num_kv_heads;
@@ -665,19 +1135,12 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
     a.num_blocks = p.num_blocks;
     a.window = p.sliding_window;
     a.max_seq_len = max_seq_len;
-    const float scale = p.scale > 0.f ? p.scale : 1.0f / sqrtf((float)p.head_dim);
     a.scale_log2 = scale * kLog2e;
     a.split_blocks = pl.split_blocks;
     a.max_splits = pl.max_splits;
     a.row_groups = pl.row_groups;
-
-    if (p.dtype == VERIFY_BF16) {
-        if (p.head_dim == 128) launch<uint16_t, 128>(a, pl, total_q, stream);
-        else launch<uint16_t, 64>(a, pl, total_q, stream);
-    } else {
-        if (p.head_dim == 128) launch<float, 128>(a, pl, total_q, stream);
-        else launch<float, 64>(a, pl, total_q, stream);
-    }
+    if (p.head_dim == 128) launch_valu<float, 128>(a, pl, total_q, stream);
+    else launch_valu<float, 64>(a, pl, total_q, stream);
     return check_launch();
 }
 

@@ -87,26 +87,36 @@ def test_attention_argument_validation(kw, want):
 
 def test_attention_workspace_query_and_checks():
     lib = av.library()
-    rc, n = _ws(_params(kv_split_blocks=8), total_q=36, max_q=9, max_s=1000)
-    assert rc == 0
-    # 63 blocks / 8 per split -> 8 splits: fp32 partial outputs and log-sum-exps
-    assert n >= 36 * 32 * 8 * (128 + 1) * 4
-    rc, n1 = _ws(_params(kv_split_blocks=1000), total_q=36, max_q=9, max_s=1000)
-    assert rc == 0 and n1 == 0          # one split: no workspace
+    # fp32 (split-K VALU path): 63 blocks / 8 per split -> 8 splits of fp32
+    # partial outputs and log-sum-exps; a single split needs no workspace
+    rc, n = _ws(_params(dtype=av.F32, kv_split_blocks=8), total_q=36, max_q=9, max_s=1000)
+    assert rc == 0 and n >= 36 * 32 * 8 * (128 + 1) * 4
+    rc, n1 = _ws(_params(dtype=av.F32, kv_split_blocks=1000), total_q=36, max_q=9, max_s=1000)
+    assert rc == 0 and n1 == 0
+    # bf16 (persistent MFMA path): per-request unit offsets plus partial slots,
+    # growing with the number of workgroups (fewer units per workgroup)
+    rc, a = _ws(_params(kv_split_blocks=64), total_q=36, max_q=9, max_s=1000)
+    rc2, b = _ws(_params(kv_split_blocks=8), total_q=36, max_q=9, max_s=1000)
+    assert rc == 0 and rc2 == 0 and 0 < a < b
+    rc, auto = _ws(_params(), total_q=36, max_q=9, max_s=1000)
+    assert rc == 0 and auto > 0
     assert lib.verify_attention_workspace_size(ctypes.byref(_params()), 36, 9, 1000, None) == av.EINVAL
     assert lib.verify_attention_workspace_size(None, 36, 9, 1000, ctypes.byref(ctypes.c_size_t())) == av.EINVAL
     # too small a workspace is refused before any launch (dummy non-null pointers)
     dummy = ctypes.c_void_p(0x1000)
-    rc = lib.verify_attention(ctypes.byref(_params(kv_split_blocks=8)), 36, 9, 1000, dummy, dummy,
-                              dummy, dummy, dummy, dummy, dummy, dummy, n - 1, None)
-    assert rc == av.EWORKSPACE
+    for kw, need in ((dict(dtype=av.F32, kv_split_blocks=8), n), (dict(kv_split_blocks=8), b)):
+        rc = lib.verify_attention(ctypes.byref(_params(**kw)), 36, 9, 1000, dummy, dummy, dummy,
+                                  dummy, dummy, dummy, dummy, dummy, need - 1, None)
+        assert rc == av.EWORKSPACE
     # null required pointers
     rc = lib.verify_attention(ctypes.byref(_params()), 36, 9, 1000, None, dummy, dummy, dummy,
-                              dummy, dummy, dummy, None, 0, None)
+                              dummy, dummy, dummy, dummy, auto, None)
     assert rc == av.EINVAL
     # negative host sizes
     assert _ws(_params(), total_q=-1)[0] == av.EINVAL
     assert _ws(_params(), max_s=-1)[0] == av.EINVAL
+    # units beyond the 32-bit unit index are refused
+    assert _ws(_params(num_seqs=65535, max_blocks_per_seq=1 << 20), max_s=1 << 24)[0] == av.EUNSUPPORTED
 
 
 def test_accept_argument_validation():
