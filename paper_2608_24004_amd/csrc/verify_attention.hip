@@ -289,6 +289,15 @@ __device__ __forceinline__ void dma16(uint32_t lds_wave_base, const void* src) {
                  : "memory", "m0");
 }
 
+// 4 bytes per lane from global memory into LDS (global_load_lds_dword): lane l
+// writes LDS bytes [lds + 4 l, lds + 4 l + 4).
+__device__ __forceinline__ void dma4(uint32_t lds_wave_base, const void* src) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_wave_base)), "v"(src)
+                 : "memory", "m0");
+}
+
 // Wait until at most N vector-memory operations of this wavefront are in flight.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -420,8 +429,15 @@ __device__ __forceinline__ void advance(const PArgs& a, const int32_t* __restric
     c.b = c.rq.b_lo;
 }
 
+// Global->LDS loads need about sixteen wavefronts per compute unit to reach
+// full HBM bandwidth, so one-tile configurations are held to four waves per
+// SIMD (at most 128 registers each).
+template <int TPW>
+constexpr int persist_waves_per_eu() { return TPW == 1 ? 4 : 2; }
+
 template <int D, int NW, int TPW, int PD>
-__global__ __launch_bounds__(NW * kWave) void attn_persist(
+__global__ __launch_bounds__(NW * kWave)
+__attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_persist(
     PArgs a, const uint16_t* __restrict__ qg, const uint8_t* __restrict__ kcg,
     const uint8_t* __restrict__ vcg, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
@@ -439,6 +455,10 @@ __global__ __launch_bounds__(NW * kWave) void attn_persist(
     static_assert(CPT * (NS - 2) < 64, "vmcnt range");
 
     __shared__ __attribute__((aligned(16))) uint8_t stage[NS][2 * TILE_BYTES];
+    // Block ids of the loader's request, blocks [wb, wb + 128) at bt_win[b & 127],
+    // refilled 64 at a time ahead of use; and whether each stage holds a valid block.
+    __shared__ int32_t bt_win[128];
+    __shared__ int32_t stage_ok[NS];
 
     const int w = blockIdx.x;
     const int U = unit_start[a.num_seqs];
@@ -481,10 +501,56 @@ __global__ __launch_bounds__(NW * kWave) void attn_persist(
     // waits below count exactly.
     const uint32_t stage_lds =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)&stage[0][0];
+    const uint32_t bt_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int32_t*)&bt_win[0];
+    int win_req = -1, wb = 0;  // block-id window of the loader (wavefront-uniform)
+    int half_base = -1;        // first block of the 64 ids cached in bt_lane
+    int bt_lane = 0;           // lane j: id of block half_base + j
+    // Entries for blocks [b0, b0 + 64) of request req (b0 a multiple of 64),
+    // loaded by wavefront 0; indices past the table row are clamped (never used).
+    auto bt_refill = [&](int req, int b0) {
+        if (wv == 0) {
+            const int idx = min(b0 + lane, a.max_blocks - 1);
+            dma4(bt_lds + (b0 & 127) * 4, block_tables + (int64_t)req * a.max_blocks + idx);
+        }
+    };
+    // Physical block of the loader's unit.  Inside a pair the loader walks
+    // blocks upwards, so the window only slides forward; a new pair (or
+    // request) restarts it synchronously.
+    auto phys_of = [&](const Cursor& c) -> int {
+        if (c.i != win_req || c.b < wb || c.b >= wb + 128) {
+            win_req = c.i;
+            wb = c.b & ~63;
+            bt_refill(c.i, wb);
+            bt_refill(c.i, wb + 64);
+            if (wv == 0) wait_vmcnt<0>();
+            if constexpr (NW > 1) lds_barrier();
+            half_base = -1;
+        } else if (c.b >= wb + 64) {
+            // blocks [wb, wb + 64) are behind the loader for good: refill their
+            // half with [wb + 128, wb + 192), needed 64 units from now
+            bt_refill(c.i, wb + 128);
+            wb += 64;
+        }
+        // One LDS read per 64 blocks brings the current half into a register;
+        // each block's id is then a readlane away.
+        if ((c.b & ~63) != half_base) {
+            half_base = c.b & ~63;
+            bt_lane = bt_win[(half_base & 127) + lane];
+        }
+        return __builtin_amdgcn_readlane(bt_lane, c.b - half_base);
+    };
+
+    // One unit = one block's K and V tiles, copied into an LDS stage with CPT
+    // global->LDS loads per thread (wavefront w's c-th load fills the 1 KiB
+    // at chunk c*NT + 64w).  Every call issues exactly CPT loads, invalid
+    // block ids reading block 0 (compute skips them through stage_ok), so the
+    // explicit vmcnt waits below count exactly.
     auto dma_unit = [&](const Cursor& c, int st) {
         const int g = c.rq.rg == 1 ? c.pq : c.pq / c.rq.rg;
-        int phys = block_tables[(int64_t)c.i * a.max_blocks + c.b];
-        phys = (phys < 0 || phys >= a.num_blocks) ? 0 : phys;
+        int phys = phys_of(c);
+        const bool ok = phys >= 0 && phys < a.num_blocks;
+        if (tid == 0) stage_ok[st] = ok;
+        phys = ok ? phys : 0;
         const int64_t off = ((int64_t)phys * a.hkv + g) * TILE_BYTES;
         const uint32_t base = stage_lds + st * (2 * TILE_BYTES);
 #pragma unroll
@@ -575,8 +641,7 @@ __global__ __launch_bounds__(NW * kWave) void attn_persist(
     };
 
     auto compute = [&](int st, int b) {
-        const int phys = block_tables[(int64_t)st_i * a.max_blocks + b];
-        if (!active || phys < 0 || phys >= a.num_blocks) return;
+        if (!active || !stage_ok[st]) return;
         const uint8_t* ks = stage[st];
         const uint8_t* vs = stage[st] + TILE_BYTES;
         f32x4_t sacc[TPW];
@@ -809,9 +874,10 @@ struct AttnPlan {
     size_t total_bytes;
 };
 
-// KV blocks in flight per workgroup: single-wavefront workers keep three
-// (24 KiB at D = 128) so that five fit a compute unit's LDS.
-constexpr int prefetch_depth(int nw) { return nw == 1 ? 3 : 4; }
+// KV blocks in flight per workgroup: three (a 32 KiB ring at D = 128), so that
+// four workgroups of four wavefronts, the sixteen wavefronts the global->LDS
+// loads need for full bandwidth, fit a compute unit's 160 KiB of LDS.
+constexpr int prefetch_depth(int) { return 3; }
 
 int validate(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
              int32_t max_seq_len) {
@@ -862,22 +928,7 @@ int resident_wgs() {
 
 template <int D>
 int resident_wgs_for(int nw, int tpw) {
-    if (nw == 1) {
-        switch (tpw) {
-            case 1: return resident_wgs<D, 1, 1>();
-            case 2: return resident_wgs<D, 1, 2>();
-            case 3: return resident_wgs<D, 1, 3>();
-            case 4: return resident_wgs<D, 1, 4>();
-        }
-        if constexpr (D == 64) {
-            switch (tpw) {
-                case 5: return resident_wgs<D, 1, 5>();
-                case 6: return resident_wgs<D, 1, 6>();
-                default: return resident_wgs<D, 1, 8>();
-            }
-        }
-        return 1;
-    }
+    if (nw == 1) return resident_wgs<D, 1, 1>();
     if constexpr (D == 128) {
         if (nw == 2) return tpw == 1 ? resident_wgs<D, 2, 1>() : resident_wgs<D, 2, 2>();
         if (nw == 4) return tpw == 1 ? resident_wgs<D, 4, 1>() : resident_wgs<D, 4, 2>();
@@ -923,8 +974,7 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
         const int tpw1_max = 1;
         if (tiles <= tpw1_max) {
             pl.nw = 1;
-            pl.tpw = (int)tiles;
-            if (p->head_dim == 64 && pl.tpw == 7) pl.tpw = 8;
+            pl.tpw = 1;
         } else {
             const int nw_max = p->head_dim == 128 ? 8 : 4;
             const int tpw_max = p->head_dim == 128 ? 2 : 4;
@@ -985,19 +1035,7 @@ void launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, hipStrea
     hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
                        m.unit_start);
     if (pl.nw == 1) {
-        switch (pl.tpw) {
-            case 1: launch_persist_k<D, 1, 1>(a, m, stream); break;
-            case 2: launch_persist_k<D, 1, 2>(a, m, stream); break;
-            case 3: launch_persist_k<D, 1, 3>(a, m, stream); break;
-            case 4: launch_persist_k<D, 1, 4>(a, m, stream); break;
-            default:
-                if constexpr (D == 64) {
-                    if (pl.tpw == 5) launch_persist_k<D, 1, 5>(a, m, stream);
-                    else if (pl.tpw == 6) launch_persist_k<D, 1, 6>(a, m, stream);
-                    else launch_persist_k<D, 1, 8>(a, m, stream);
-                }
-                break;
-        }
+        launch_persist_k<D, 1, 1>(a, m, stream);
     } else if constexpr (D == 128) {
         if (pl.nw == 2) {
             if (pl.tpw == 1) launch_persist_k<D, 2, 1>(a, m, stream);
