@@ -24,6 +24,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E datasheet peak
+CALIB_BYTES = 256 << 20  # the plain elementwise kernel of --copy-calibration reads and writes this
+# sources whose change invalidates a stored traffic measurement of the attention call
+KERNEL_SOURCES = ("paper_2608_24004_amd/csrc/verify_attention.hip",
+                  "paper_2608_24004_amd/csrc/common.h", "paper_2608_24004_amd/build.py")
 
 
 def log(*a):
@@ -52,6 +56,90 @@ def accept_bytes(bt) -> float:
     e = 2 if cfg.dtype == "bf16" else 4
     T, B = bt.total_q, len(bt.seq_lens)
     return float(T) * cfg.vocab * e + 4.0 * (4 * T + 3 * B + 1)
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", "traffic_verify_attention_%s.txt" % workload)
+
+
+def stored_traffic(workload: str):
+    """HBM bytes per verify_attention call from the committed counter summary,
+    or None when there is none or the kernel sources changed since it was taken."""
+    try:
+        kv = dict(l.split(":", 1) for l in open(traffic_file(workload)) if ":" in l)
+    except OSError:
+        return None
+    if kv.get("source_sha256", "").strip() != kernel_source_hash():
+        return None
+    return float(kv["traffic_bytes_per_call"])
+
+
+def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
+    """Turn two rocprofv3 --pmc runs of `bench.py --copy-calibration` (FETCH_SIZE,
+    then WRITE_SIZE; KiB per dispatch) into HBM bytes per verify_attention call.
+    Each counter is scaled by what it reads for the calibration kernel, which
+    moves CALIB_BYTES in each direction.  Prints the summary text."""
+    import collections
+    import csv
+    import re
+
+    def per_kernel(path, counter):
+        by_dispatch = collections.defaultdict(float)
+        names = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = r["Dispatch_Id"]
+            by_dispatch[d] += float(r["Counter_Value"])
+            names[d] = r["Kernel_Name"]
+        groups = collections.defaultdict(list)
+        calib = None
+        for d in sorted(by_dispatch, key=int):
+            n = names[d]
+            m = re.search(r"averify::\(anonymous namespace\)::(\w+)", n)
+            if m:
+                groups[m.group(1)].append(by_dispatch[d])
+            elif "bitwise_not" in n:
+                calib = by_dispatch[d]
+        return {k: sum(v) / len(v) for k, v in groups.items()}, \
+               {k: len(v) for k, v in groups.items()}, calib
+
+    fk, fn, fcal = per_kernel(fetch_csv, "FETCH_SIZE")
+    wk, wn, wcal = per_kernel(write_csv, "WRITE_SIZE")
+    if not fcal or not wcal:
+        raise SystemExit("no calibration dispatch (run bench.py with --copy-calibration)")
+    ff = CALIB_BYTES / (fcal * 1024.0)
+    wf = CALIB_BYTES / (wcal * 1024.0)
+    attn = [k for k in fk if k.startswith("attn_")]
+    total = 0.0
+    lines = []
+    for k in sorted(attn):
+        fb = fk[k] * 1024.0 * ff
+        wb = wk.get(k, 0.0) * 1024.0 * wf
+        total += fb + wb
+        lines.append("  %-22s dispatches %3d  FETCH %10.1f KiB  WRITE %9.1f KiB  -> %.4f GB read, "
+                     "%.4f GB written" % (k, fn[k], fk[k], wk.get(k, 0.0), fb / 1e9, wb / 1e9))
+    for k in sorted(set(fk) - set(attn)):
+        lines.append("  %-22s dispatches %3d  FETCH %10.1f KiB  WRITE %9.1f KiB  (not attention)" % (
+            k, fn[k], fk[k], wk.get(k, 0.0)))
+    print("workload: %s" % workload)
+    print("source_sha256: %s" % kernel_source_hash())
+    print("traffic_bytes_per_call: %.0f" % total)
+    print("calibration_fetch_factor: %.4f" % ff)
+    print("calibration_write_factor: %.4f" % wf)
+    print("calibration: bitwise_not over %d MiB int32 reads %.1f KiB, writes %.1f KiB" % (
+        CALIB_BYTES >> 20, fcal, wcal))
+    print("per-kernel mean per dispatch:")
+    print("\n".join(lines))
 
 
 def cpu_baseline(bt, budget_s: float):
@@ -114,7 +202,16 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run one plain elementwise kernel that reads "
+                         "and writes %d MiB (scale for the HBM byte counters)" % (CALIB_BYTES >> 20))
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the HBM traffic summary of two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.config)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the verify step runs on a single MI355X "
@@ -206,6 +303,19 @@ def main():
     log("drafts proposed %d accepted %d (rejection rate %.3f), emitted %d, scored positions %d" % (
         proposed, accepted, 1 - accepted / max(1, proposed), emitted, T))
 
+    if args.copy_calibration:
+        x = torch.zeros(CALIB_BYTES // 4, dtype=torch.int32, device=dev)
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        torch.bitwise_not(x, out=y)
+        torch.cuda.synchronize()
+        del x, y
+
+    traffic = stored_traffic(cfg.name)
+    if traffic is not None:
+        log("HBM traffic per attention call (counters): %.4f GB vs algorithmic %.4f GB" % (
+            traffic / 1e9, abytes[dom] / 1e9))
+
     cpu = None
     if args.cpu_budget > 0:
         log("cpu baseline (oracle) ...")
@@ -231,8 +341,10 @@ def main():
                    "head_dim": cfg.head_dim, "vocab": cfg.vocab, "layers": len(bt.layers),
                    "seed": args.seed},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "verify_attention (layer %d)" % dom},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "algorithmic_bytes": abytes[dom],
+                     "kernel": "verify_attention call (attn_schedule + attn_persist + "
+                               "attn_combine_slots), layer %d" % dom},
         "step_hbm_frac": step_bytes / ms_step / 1e6 / HBM_PEAK_GBS,
         "scored_positions_per_s": T / (ms_step * 1e-3),
         "rejection_rate": 1 - accepted / max(1, proposed),

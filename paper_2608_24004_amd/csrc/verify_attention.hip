@@ -247,10 +247,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
 //
 // Inside a workgroup the NW wavefronts split the pair's query rows (TPW tiles
 // of 16 rows each) and share the KV blocks: each block's K and V tiles (16
-// tokens x D, contiguous in the paged layout) are loaded once with 16-byte
-// coalesced loads, PD blocks ahead, into registers, written to a
-// double-buffered LDS ring and read by every wavefront as MFMA operands.
-// The load stream runs straight across pair boundaries.
+// tokens x D, contiguous in the paged layout) are copied once, 16 bytes per
+// lane, straight from global memory into a ring of PD + 1 LDS stages (PD
+// blocks in flight), and read from there by every wavefront as MFMA operands.
+// The load stream runs straight across pair boundaries; the block ids it
+// needs are staged in an LDS window ahead of it.
 //
 // Per block and 16-row tile, with lane = 16*lg + l16:
 //   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K (16 keys x 32 dims, lane
@@ -494,11 +495,6 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
         c0.b = c0.rq.b_lo + (off - c0.pq * c0.rq.nb);
     }
 
-    // One unit = one block's K and V tiles, copied into an LDS stage with CPT
-    // global->LDS loads per thread (wavefront w's c-th load fills the 1 KiB
-    // at chunk c*NT + 64w).  Every call issues exactly CPT loads, invalid
-    // block ids reading block 0 (compute skips them), so the explicit vmcnt
-    // waits below count exactly.
     const uint32_t stage_lds =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)&stage[0][0];
     const uint32_t bt_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int32_t*)&bt_win[0];
