@@ -299,6 +299,21 @@ __device__ __forceinline__ void dma4(uint32_t lds_wave_base, const void* src) {
                  : "memory", "m0");
 }
 
+// Maximum of v over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes that hold
+// one row of an MFMA result tile).  Each permlane swap exchanges half of the
+// wavefront between its two operands; with both operands equal to v, the two
+// results of lane l are v of l and of l ^ 32 (l ^ 16), in some order.
+__device__ __forceinline__ float row_max_4lanes(float v) {
+    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// Softmax weights may exceed 1 by up to this factor (log2) before the stored
+// row maximum is raised.
+constexpr float kSlackLog2 = 8.f;
+
 // Wait until at most N vector-memory operations of this wavefront are in flight.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -319,6 +334,7 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) { return __builtin
 struct PArgs {
     int num_seqs, hq, hkv, group, max_blocks, num_blocks, window, max_seq_len;
     float scale_log2;
+    float inv_scale_log2;  // 1 / scale_log2 (0 when the scale is 0)
     int rows_per_group;   // NW * TPW * 16
     int rg_max;           // row groups per (request, KV head) at most
     int nwg;              // workgroups of the persistent launch
@@ -457,9 +473,8 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
 
     __shared__ __attribute__((aligned(16))) uint8_t stage[NS][2 * TILE_BYTES];
     // Block ids of the loader's request, blocks [wb, wb + 128) at bt_win[b & 127],
-    // refilled 64 at a time ahead of use; and whether each stage holds a valid block.
+    // refilled 64 at a time ahead of use.
     __shared__ int32_t bt_win[128];
-    __shared__ int32_t stage_ok[NS];
 
     const int w = blockIdx.x;
     const int U = unit_start[a.num_seqs];
@@ -539,13 +554,16 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     // One unit = one block's K and V tiles, copied into an LDS stage with CPT
     // global->LDS loads per thread (wavefront w's c-th load fills the 1 KiB
     // at chunk c*NT + 64w).  Every call issues exactly CPT loads, invalid
-    // block ids reading block 0 (compute skips them through stage_ok), so the
+    // block ids reading block 0 (compute skips them through ok_mask), so the
     // explicit vmcnt waits below count exactly.
+    // Bit s: stage s holds a valid block.  Every wavefront runs the same
+    // loader steps, so each keeps its own copy in a scalar register.
+    uint32_t ok_mask = 0;
     auto dma_unit = [&](const Cursor& c, int st) {
         const int g = c.rq.rg == 1 ? c.pq : c.pq / c.rq.rg;
         int phys = phys_of(c);
         const bool ok = phys >= 0 && phys < a.num_blocks;
-        if (tid == 0) stage_ok[st] = ok;
+        ok_mask = ok ? (ok_mask | (1u << st)) : (ok_mask & ~(1u << st));
         phys = ok ? phys : 0;
         const int64_t off = ((int64_t)phys * a.hkv + g) * TILE_BYTES;
         const uint32_t base = stage_lds + st * (2 * TILE_BYTES);
@@ -565,7 +583,11 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     bf16x8_t qop[TPW][KC];
     int row_j[TPW];
     f32x4_t o[TPW][DT];
-    float m_r[TPW], l_r[TPW];
+    // Online softmax state per tile, in the log2 domain: m_r is the maximum
+    // the row's exponentials are taken against (identical in the four lanes
+    // that hold the row), thr the raw score above which a lane needs a new
+    // maximum, neg_m = -m_r (0 while the row has seen no key).
+    float m_r[TPW], l_r[TPW], thr[TPW], neg_m[TPW];
 
     auto init_pair = [&](const Cursor& c) {
         st_i = c.i;
@@ -591,6 +613,8 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
             }
             m_r[t] = -INFINITY;
             l_r[t] = 0.f;
+            thr[t] = -INFINITY;
+            neg_m[t] = 0.f;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
@@ -637,7 +661,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     };
 
     auto compute = [&](int st, int b) {
-        if (!active || !stage_ok[st]) return;
+        if (!active || !((ok_mask >> st) & 1u)) return;
         const uint8_t* ks = stage[st];
         const uint8_t* vs = stage[st] + TILE_BYTES;
         f32x4_t sacc[TPW];
@@ -660,9 +684,9 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
         i16x4_t pop[TPW];
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
-            float sv[4];
+            float sv[4];  // raw scores <q, k> of keys key0 .. key0 + 3
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sv[r] = sacc[t][r] * a.scale_log2;
+            for (int r = 0; r < 4; ++r) sv[r] = sacc[t][r];
             if (need_mask) {
                 const int p = p_first + row_j[t];
 #pragma unroll
@@ -672,29 +696,34 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
                     sv[r] = vis ? sv[r] : -INFINITY;
                 }
             }
-            float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float mnew = fmaxf(m_r[t], mx);
-            const float muse = mnew == -INFINITY ? 0.f : mnew;
-            // exponent arguments are <= 0: the raw v_exp_f32 is exact enough
-            // and results below 2^-126 only flush to zero
-            const float alpha = __builtin_amdgcn_exp2f(m_r[t] - muse);
+            // The exponentials are taken against the stored maximum m_r as long
+            // as no score exceeds it by more than 2^kSlackLog2; only then (on a
+            // row's first keys, and rarely after) does the wavefront reduce
+            // the new row maximum over the row's four lanes and rescale.  The
+            // weights stay below 2^kSlackLog2, and bf16 rounds them with the
+            // same relative error at any magnitude.
+            const float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+            if (__builtin_amdgcn_ballot_w64(!(mx <= thr[t]))) {
+                const float rmax = row_max_4lanes(mx) * a.scale_log2;
+                if (rmax > m_r[t]) {
+                    // m_r = -inf: nothing accumulated yet, alpha = 0 keeps it 0
+                    const float alpha = __builtin_amdgcn_exp2f(m_r[t] - rmax);
+                    l_r[t] *= alpha;
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
+                    m_r[t] = rmax;
+                    neg_m[t] = -rmax;
+                    thr[t] = (rmax + kSlackLog2) * a.inv_scale_log2;
+                }
+            }
+            // exponent arguments are <= kSlackLog2: the raw v_exp_f32 is exact
+            // enough and results below 2^-126 only flush to zero
             float pr[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(sv[r] - muse);
-            l_r[t] = l_r[t] * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
-            // The accumulated output only needs rescaling when a row's running
-            // maximum grew (and it already held something); after the first
-            // blocks that is rare, so test it once for the whole wavefront.
-            const bool grew = alpha != 1.f && m_r[t] != -INFINITY;
-            m_r[t] = mnew;
+            for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[r], a.scale_log2, neg_m[t]));
+            l_r[t] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
             pop[t] = __builtin_bit_cast(i16x4_t, make_uint2(pack_bf16x2(pr[0], pr[1]),
                                                             pack_bf16x2(pr[2], pr[3])));
-            if (__builtin_amdgcn_ballot_w64(grew)) {
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
-            }
         }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
@@ -870,10 +899,42 @@ struct AttnPlan {
     size_t total_bytes;
 };
 
-// KV blocks in flight per workgroup: three (a 32 KiB ring at D = 128), so that
-// four workgroups of four wavefronts, the sixteen wavefronts the global->LDS
-// loads need for full bandwidth, fit a compute unit's 160 KiB of LDS.
-constexpr int prefetch_depth(int) { return 3; }
+// KV blocks in flight per workgroup.  Three (a 32 KiB ring at D = 128) lets
+// four workgroups share a compute unit's 160 KiB of LDS; the four-wavefront
+// two-tile shape runs two workgroups per compute unit (its registers allow no
+// more) and takes five.  More workgroups per compute unit beat deeper rings:
+// each workgroup advances one block per barrier, so the per-block latency of
+// one workgroup is what more workgroups hide.
+constexpr int prefetch_depth(int d, int nw, int tpw) { return d == 128 && nw == 4 && tpw == 2 ? 5 : 3; }
+
+// The kernel shapes a plan may choose: head dim, wavefronts per workgroup,
+// 16-row tiles per wavefront.  with_shape calls f(Shape<...>{}) for the
+// matching entry and returns false if there is none.
+template <int D_, int NW_, int TPW_>
+struct Shape {
+    static constexpr int D = D_, NW = NW_, TPW = TPW_, PD = prefetch_depth(D_, NW_, TPW_);
+};
+
+template <typename F>
+bool with_shape(int d, int nw, int tpw, F&& f) {
+#define AVERIFY_SHAPE(D_, NW_, TPW_)                       \
+    if (d == D_ && nw == NW_ && tpw == TPW_) {             \
+        f(Shape<D_, NW_, TPW_>{});                         \
+        return true;                                       \
+    }
+    AVERIFY_SHAPE(128, 1, 1)
+    AVERIFY_SHAPE(128, 2, 1)
+    AVERIFY_SHAPE(128, 2, 2)
+    AVERIFY_SHAPE(128, 4, 2)
+    AVERIFY_SHAPE(64, 1, 1)
+    AVERIFY_SHAPE(64, 2, 1)
+    AVERIFY_SHAPE(64, 4, 1)
+    AVERIFY_SHAPE(64, 4, 2)
+    AVERIFY_SHAPE(64, 4, 3)
+    AVERIFY_SHAPE(64, 4, 4)
+#undef AVERIFY_SHAPE
+    return false;
+}
 
 int validate(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
              int32_t max_seq_len) {
@@ -906,45 +967,20 @@ int device_cus() {
     return v;
 }
 
-template <int D, int NW, int TPW>
+template <typename S>
 int resident_wgs() {
     static std::atomic<int> cache[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 2; }
     int v = cache[dev].load(std::memory_order_relaxed);
     if (v > 0) return v;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, attn_persist<D, NW, TPW, prefetch_depth(NW)>,
-                                                     NW * kWave, 0) != hipSuccess || v <= 0) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, attn_persist<S::D, S::NW, S::TPW, S::PD>,
+                                                     S::NW * kWave, 0) != hipSuccess || v <= 0) {
         (void)hipGetLastError();
         v = 1;
     }
     cache[dev].store(v, std::memory_order_relaxed);
     return v;
-}
-
-template <int D>
-int resident_wgs_for(int nw, int tpw) {
-    if (nw == 1) return resident_wgs<D, 1, 1>();
-    if constexpr (D == 128) {
-        if (nw == 2) return tpw == 1 ? resident_wgs<D, 2, 1>() : resident_wgs<D, 2, 2>();
-        if (nw == 4) return tpw == 1 ? resident_wgs<D, 4, 1>() : resident_wgs<D, 4, 2>();
-        return tpw == 1 ? resident_wgs<D, 8, 1>() : resident_wgs<D, 8, 2>();
-    } else {
-        if (nw == 2) {
-            switch (tpw) {
-                case 1: return resident_wgs<D, 2, 1>();
-                case 2: return resident_wgs<D, 2, 2>();
-                case 3: return resident_wgs<D, 2, 3>();
-                default: return resident_wgs<D, 2, 4>();
-            }
-        }
-        switch (tpw) {
-            case 1: return resident_wgs<D, 4, 1>();
-            case 2: return resident_wgs<D, 4, 2>();
-            case 3: return resident_wgs<D, 4, 3>();
-            default: return resident_wgs<D, 4, 4>();
-        }
-    }
 }
 
 int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
@@ -962,21 +998,23 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
     if (pl.mfma) {
         // A single tile goes to single-wavefront workgroups: every wavefront is
         // an independent worker with its own LDS ring and no barrier.  More
-        // rows use NW wavefronts sharing one ring, one or two tiles each (a
-        // wavefront holding all tiles runs at one wave per SIMD and cannot hide
-        // its latencies); NW divides the 16-byte chunks of a block (512 at
-        // D = 128, 256 at D = 64) so every thread loads alike.
+        // rows use NW wavefronts sharing one ring (NW divides the 16-byte
+        // chunks of a block, 512 at D = 128 and 256 at D = 64, so every thread
+        // loads alike).  At D = 128 a wavefront takes two tiles once there are
+        // three or more: fewer wavefronts per block mean fewer barriers and
+        // more workgroups per compute unit, which is what hides the per-block
+        // latency of the online softmax.  Rows beyond the shape's reach are
+        // split into row groups, each walking the request's KV again.
         const int64_t tiles = (rows + 15) / 16;
-        const int tpw1_max = 1;
-        if (tiles <= tpw1_max) {
+        if (tiles <= 1) {
             pl.nw = 1;
             pl.tpw = 1;
+        } else if (p->head_dim == 128) {
+            pl.nw = tiles <= 4 ? 2 : 4;
+            pl.tpw = tiles == 2 ? 1 : 2;
         } else {
-            const int nw_max = p->head_dim == 128 ? 8 : 4;
-            const int tpw_max = p->head_dim == 128 ? 2 : 4;
-            pl.nw = 2;
-            while (pl.nw < nw_max && pl.nw < tiles) pl.nw *= 2;
-            pl.tpw = (int)std::min<int64_t>(tpw_max, (tiles + pl.nw - 1) / pl.nw);
+            pl.nw = tiles <= 2 ? 2 : 4;
+            pl.tpw = (int)std::min<int64_t>(4, (tiles + pl.nw - 1) / pl.nw);
         }
         const int64_t per = (int64_t)pl.nw * pl.tpw * 16;
         pl.rg_max = (int)((rows + per - 1) / per);
@@ -987,8 +1025,9 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
         if (pl.spb > 0) {
             pl.nwg = (int)std::min<int64_t>((units_max + pl.spb - 1) / pl.spb, (int64_t)1 << 30);
         } else {
-            const int res = p->head_dim == 128 ? resident_wgs_for<128>(pl.nw, pl.tpw)
-                                               : resident_wgs_for<64>(pl.nw, pl.tpw);
+            int res = 0;
+            if (!with_shape(p->head_dim, pl.nw, pl.tpw, [&](auto sh) { res = resident_wgs<decltype(sh)>(); }))
+                return VERIFY_EUNSUPPORTED;
             pl.nwg = device_cus() * res;
         }
         pl.slots = pairs + pl.nwg;
@@ -1019,52 +1058,25 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
     return VERIFY_OK;
 }
 
-template <int D, int NW, int TPW>
-void launch_persist_k(const PArgs& a, const MPtrs& m, hipStream_t stream) {
-    hipLaunchKernelGGL((attn_persist<D, NW, TPW, prefetch_depth(NW)>), dim3(a.nwg), dim3(NW * kWave), 0,
-                       stream, a, m.q, m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start,
-                       m.unit_start, m.out, m.slot_o, m.slot_lse);
-}
-
-template <int D>
-void launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, hipStream_t stream) {
+// Schedule pass, then the persistent kernel of the plan's shape, then the
+// merge of partial slots.  Returns false if the plan names no known shape.
+bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, int head_dim,
+                    hipStream_t stream) {
     hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
                        m.unit_start);
-    if (pl.nw == 1) {
-        launch_persist_k<D, 1, 1>(a, m, stream);
-    } else if constexpr (D == 128) {
-        if (pl.nw == 2) {
-            if (pl.tpw == 1) launch_persist_k<D, 2, 1>(a, m, stream);
-            else launch_persist_k<D, 2, 2>(a, m, stream);
-        } else if (pl.nw == 4) {
-            if (pl.tpw == 1) launch_persist_k<D, 4, 1>(a, m, stream);
-            else launch_persist_k<D, 4, 2>(a, m, stream);
-        } else {
-            if (pl.tpw == 1) launch_persist_k<D, 8, 1>(a, m, stream);
-            else launch_persist_k<D, 8, 2>(a, m, stream);
-        }
-    } else {
-        if (pl.nw == 2) {
-            switch (pl.tpw) {
-                case 1: launch_persist_k<D, 2, 1>(a, m, stream); break;
-                case 2: launch_persist_k<D, 2, 2>(a, m, stream); break;
-                case 3: launch_persist_k<D, 2, 3>(a, m, stream); break;
-                default: launch_persist_k<D, 2, 4>(a, m, stream); break;
-            }
-        } else {
-            switch (pl.tpw) {
-                case 1: launch_persist_k<D, 4, 1>(a, m, stream); break;
-                case 2: launch_persist_k<D, 4, 2>(a, m, stream); break;
-                case 3: launch_persist_k<D, 4, 3>(a, m, stream); break;
-                default: launch_persist_k<D, 4, 4>(a, m, stream); break;
-            }
-        }
-    }
-    const int64_t pairs = (int64_t)a.num_seqs * a.hkv * a.rg_max;
-    constexpr int rpb = kCombineThreads / (D / 4);
-    const int chunks = (a.rows_per_group + rpb - 1) / rpb;
-    hipLaunchKernelGGL((attn_combine_slots<D>), dim3((unsigned)pairs, chunks), dim3(kCombineThreads),
-                       0, stream, a, m.seq_lens, m.q_start, m.unit_start, m.slot_o, m.slot_lse, m.out);
+    return with_shape(head_dim, pl.nw, pl.tpw, [&](auto sh) {
+        using S = decltype(sh);
+        hipLaunchKernelGGL((attn_persist<S::D, S::NW, S::TPW, S::PD>), dim3(a.nwg), dim3(S::NW * kWave), 0,
+                           stream, a, m.q, m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start,
+                           m.unit_start, m.out, m.slot_o, m.slot_lse);
+        const int64_t pairs = (int64_t)a.num_seqs * a.hkv * a.rg_max;
+        constexpr int RPB = kCombineThreads / (S::D / 4);
+        const unsigned chunks = (unsigned)((a.rows_per_group + RPB - 1) / RPB);
+        if (pairs > 0)
+            hipLaunchKernelGGL((attn_combine_slots<S::D>), dim3((unsigned)pairs, chunks),
+                               dim3(kCombineThreads), 0, stream, a, m.seq_lens, m.q_start,
+                               m.unit_start, m.slot_o, m.slot_lse, m.out);
+    });
 }
 
 template <typename T, int D>
@@ -1140,12 +1152,12 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         a.window = p.sliding_window;
         a.max_seq_len = max_seq_len;
         a.scale_log2 = scale * kLog2e;
+        a.inv_scale_log2 = a.scale_log2 > 0.f ? 1.f / a.scale_log2 : 0.f;
         a.rows_per_group = pl.nw * pl.tpw * 16;
         a.rg_max = pl.rg_max;
         a.nwg = pl.nwg;
         a.spb = pl.spb;
-        if (p.head_dim == 128) launch_persist<128>(a, m, pl, stream);
-        else launch_persist<64>(a, m, pl, stream);
+        if (!launch_persist(a, m, pl, p.head_dim, stream)) return VERIFY_EUNSUPPORTED;
         return check_launch();
     }
 
