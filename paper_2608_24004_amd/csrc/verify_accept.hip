@@ -92,14 +92,29 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_chunks(
     if ((reinterpret_cast<uintptr_t>(rowp + lo) & 15u) == 0) {
         const uint4* vp = reinterpret_cast<const uint4*>(rowp + lo);
         const int64_t nvec = (hi - lo) / E;
+        // Batches of kArgmaxUnroll vectors per thread, the next batch loaded
+        // before the current one is scanned so that loads stay in flight
+        // while the wavefront compares.
+        constexpr int64_t kStep = (int64_t)kArgmaxUnroll * kArgmaxThreads;
         int64_t vi = tid;
-        for (; vi + (kArgmaxUnroll - 1) * kArgmaxThreads < nvec; vi += kArgmaxUnroll * kArgmaxThreads) {
-            uint4 v[kArgmaxUnroll];
+        if (vi + (kArgmaxUnroll - 1) * kArgmaxThreads < nvec) {
+            uint4 cur[kArgmaxUnroll];
 #pragma unroll
-            for (int u = 0; u < kArgmaxUnroll; ++u) v[u] = ld16_stream(vp + vi + u * kArgmaxThreads);
+            for (int u = 0; u < kArgmaxUnroll; ++u) cur[u] = ld16_stream(vp + vi + u * kArgmaxThreads);
+            for (; vi + kStep + (kArgmaxUnroll - 1) * kArgmaxThreads < nvec; vi += kStep) {
+                uint4 nxt[kArgmaxUnroll];
+#pragma unroll
+                for (int u = 0; u < kArgmaxUnroll; ++u) nxt[u] = ld16_stream(vp + vi + kStep + u * kArgmaxThreads);
+#pragma unroll
+                for (int u = 0; u < kArgmaxUnroll; ++u)
+                    scan_vec<T>(cur[u], (uint32_t)(lo + (vi + u * kArgmaxThreads) * E), best, best_idx, nan_idx);
+#pragma unroll
+                for (int u = 0; u < kArgmaxUnroll; ++u) cur[u] = nxt[u];
+            }
 #pragma unroll
             for (int u = 0; u < kArgmaxUnroll; ++u)
-                scan_vec<T>(v[u], (uint32_t)(lo + (vi + u * kArgmaxThreads) * E), best, best_idx, nan_idx);
+                scan_vec<T>(cur[u], (uint32_t)(lo + (vi + u * kArgmaxThreads) * E), best, best_idx, nan_idx);
+            vi += kStep;
         }
         for (; vi < nvec; vi += kArgmaxThreads) {
             uint4 v = ld16_stream(vp + vi);
@@ -200,10 +215,19 @@ struct AcceptPlan {
     size_t argmax_bytes;  // scratch argmax when the caller passes none
 };
 
+// Rows are cut into chunks so that the whole grid is about one round of
+// resident workgroups (eight 256-thread workgroups on each of MI355X's 256
+// compute units): a second, partly filled round would leave most of the chip
+// idle for its duration.  Chunks are whole 16-byte vectors per thread.
+constexpr int64_t kArgmaxTargetWgs = 2048;
+
 AcceptPlan plan_accept(int32_t total_q, int64_t vocab, int32_t dtype) {
     AcceptPlan p{};
     const int per16 = dtype == VERIFY_BF16 ? 8 : 4;
-    p.chunk_elems = (int64_t)kArgmaxThreads * kArgmaxUnroll * per16 * 2;
+    const int64_t quantum = (int64_t)kArgmaxThreads * per16;
+    const int64_t want = std::max<int64_t>(1, kArgmaxTargetWgs / std::max<int64_t>(1, total_q));
+    const int64_t per_chunk = (vocab + want - 1) / want;
+    p.chunk_elems = (per_chunk + quantum - 1) / quantum * quantum;
     p.nchunks = (int)((vocab + p.chunk_elems - 1) / p.chunk_elems);
     p.partial_bytes = align_up((size_t)total_q * p.nchunks * sizeof(uint64_t), 256);
     p.argmax_bytes = align_up((size_t)total_q * sizeof(int32_t), 256);

@@ -250,8 +250,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
 // tokens x D, contiguous in the paged layout) are copied once, 16 bytes per
 // lane, straight from global memory into a ring of PD + 1 LDS stages (PD
 // blocks in flight), and read from there by every wavefront as MFMA operands.
-// The load stream runs straight across pair boundaries; the block ids it
-// needs are staged in an LDS window ahead of it.
+// The load stream runs straight across pair boundaries; the block id of each
+// block it loads is a scalar load issued one block earlier.
 //
 // Per block and 16-row tile, with lane = 16*lg + l16:
 //   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K (16 keys x 32 dims, lane
@@ -290,14 +290,6 @@ __device__ __forceinline__ void dma16(uint32_t lds_wave_base, const void* src) {
                  : "memory", "m0");
 }
 
-// 4 bytes per lane from global memory into LDS (global_load_lds_dword): lane l
-// writes LDS bytes [lds + 4 l, lds + 4 l + 4).
-__device__ __forceinline__ void dma4(uint32_t lds_wave_base, const void* src) {
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
-                 :
-                 : "s"(__builtin_amdgcn_readfirstlane(lds_wave_base)), "v"(src)
-                 : "memory", "m0");
-}
 
 // Maximum of v over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes that hold
 // one row of an MFMA result tile).  Each permlane swap exchanges half of the
@@ -339,6 +331,7 @@ struct PArgs {
     int rg_max;           // row groups per (request, KV head) at most
     int nwg;              // workgroups of the persistent launch
     int spb;              // > 0: fixed number of units per workgroup
+    int inline_sched;     // 1: attn_persist computes the unit offsets itself
 };
 
 struct MPtrs {
@@ -429,7 +422,7 @@ __global__ __launch_bounds__(1024) void attn_schedule(PArgs a, const int32_t* __
 }
 
 struct Cursor {
-    int i, pq, b;  // request, pair within the request (head * rg + row group), block
+    int i, g, r, b;  // request, KV head, row group, block
     ReqGeom rq;
 };
 
@@ -437,13 +430,141 @@ __device__ __forceinline__ void advance(const PArgs& a, const int32_t* __restric
                                         const int32_t* __restrict__ seq_lens, Cursor& c) {
     if (++c.b < c.rq.b_lo + c.rq.nb) return;
     c.b = c.rq.b_lo;
-    if (++c.pq < a.hkv * c.rq.rg) return;
-    c.pq = 0;
+    if (++c.r < c.rq.rg) return;
+    c.r = 0;
+    if (++c.g < a.hkv) return;
+    c.g = 0;
     while (++c.i < a.num_seqs) {
         c.rq = req_geom(a, q_start, seq_lens, c.i);
         if (c.rq.rg > 0 && c.rq.nb > 0) break;
     }
     c.b = c.rq.b_lo;
+}
+
+// Batches of at most this many requests are scheduled inside attn_persist:
+// every workgroup computes the per-request unit offsets itself (a scan over
+// the batch's metadata, cheaper than a separate launch), and workgroup 0
+// also stores them for the merge pass.
+constexpr int kInlineSchedSeqs = 256;
+
+// Exclusive prefix over the batch of each request's units (Hkv * row groups *
+// blocks) into sched[0 .. num_seqs], sched[num_seqs] = total; one wavefront.
+__device__ __forceinline__ void sched_prefix(const PArgs& a, const int32_t* __restrict__ q_start,
+                                             const int32_t* __restrict__ seq_lens, int32_t* sched,
+                                             int lane) {
+    int carry = 0;
+    for (int base = 0; base < a.num_seqs; base += kWave) {
+        const int i = base + lane;
+        int u = 0;
+        if (i < a.num_seqs) {
+            const ReqGeom r = req_geom(a, q_start, seq_lens, i);
+            u = a.hkv * r.rg * r.nb;
+        }
+        int x = u;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        if (i < a.num_seqs) sched[i] = carry + x - u;
+        carry += __shfl(x, kWave - 1);
+    }
+    if (lane == 0) sched[a.num_seqs] = carry;
+}
+
+// Unit range [us, ue) of workgroup w (empty when w has none).
+__device__ __forceinline__ void unit_range(const PArgs& a, int U, int w, int& us, int& ue) {
+    if (a.spb > 0) {
+        us = (int)min((int64_t)U, (int64_t)w * a.spb);
+        ue = (int)min((int64_t)U, (int64_t)us + a.spb);
+    } else {
+        const int n = sharing_wgs(a, U);
+        us = w < n ? (int)((int64_t)U * w / n) : U;
+        ue = w < n ? (int)((int64_t)U * (w + 1) / n) : U;
+    }
+}
+
+// Value of a wavefront-uniform load, marked uniform for the compiler (a load
+// through LDS or a pointer the kernel also writes is otherwise taken as
+// divergent, and so is everything computed from it).
+__device__ __forceinline__ int uniform_load(const int32_t* p) { return __builtin_amdgcn_readfirstlane(*p); }
+
+// Cursor of unit u: its request is the largest i with unit_start[i] <= u.
+__device__ __forceinline__ Cursor locate_unit(const PArgs& a, const int32_t* __restrict__ q_start,
+                                              const int32_t* __restrict__ seq_lens,
+                                              const int32_t* unit_start, int u) {
+    int lo = 0, hi = a.num_seqs - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (uniform_load(unit_start + mid) <= u) lo = mid; else hi = mid - 1;
+    }
+    Cursor c;
+    c.i = lo;
+    c.rq = req_geom(a, q_start, seq_lens, lo);
+    const int off = u - uniform_load(unit_start + lo);
+    const int pq = off / c.rq.nb;  // pair within the request: head * rg + row group
+    c.g = pq / c.rq.rg;
+    c.r = pq - c.g * c.rq.rg;
+    c.b = c.rq.b_lo + (off - pq * c.rq.nb);
+    return c;
+}
+
+// One online-softmax step of a 16-row tile over one 16-key block.  sacc holds
+// raw scores <q, k> in the MFMA result layout (lane 16 lg + l16: keys
+// key0 .. key0 + 3 of the tile's row l16, key0 = 16 b + 4 lg); row_j is the
+// row's draft position (-1: no row) and p_first the position of the request's
+// first row.  The exponentials are taken against the stored maximum m as long
+// as no score exceeds it by more than 2^kSlackLog2; only then (on a row's
+// first keys, and rarely after) does the wavefront reduce the new row maximum
+// over the row's four lanes and rescale l and o.  The weights stay below
+// 2^kSlackLog2, and bf16 rounds them with the same relative error at any
+// magnitude.  Returns the weights as the bf16 B operand of the PV product.
+template <int DT>
+__device__ __forceinline__ i16x4_t softmax_step(const f32x4_t& sacc, bool need_mask, int row_j,
+                                                int p_first, int key0, int window, float c,
+                                                float inv_c, float& m, float& l, float& thr,
+                                                float& neg_m, f32x4_t (&o)[DT]) {
+    float sv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sv[r] = sacc[r];
+    if (need_mask) {
+        const int p = p_first + row_j;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int key = key0 + r;
+            const bool vis = row_j >= 0 && key <= p && (window == 0 || key > p - window);
+            sv[r] = vis ? sv[r] : -INFINITY;
+        }
+    }
+    const float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    if (__builtin_amdgcn_ballot_w64(!(mx <= thr))) {
+        const float rmax = row_max_4lanes(mx) * c;
+        if (rmax > m) {
+            // m = -inf: nothing accumulated yet, alpha = 0 keeps it 0
+            const float alpha = __builtin_amdgcn_exp2f(m - rmax);
+            l *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+            m = rmax;
+            neg_m = -rmax;
+            thr = (rmax + kSlackLog2) * inv_c;
+        }
+    }
+    // exponent arguments are <= kSlackLog2: the raw v_exp_f32 is exact enough
+    // and results below 2^-126 only flush to zero
+    float pr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[r], c, neg_m));
+    l += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+    return __builtin_bit_cast(i16x4_t, make_uint2(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3])));
+}
+
+// Whether every row of the request sees every key of block b: the block lies
+// below the first row's position and, with a window, inside the last row's
+// window.
+__device__ __forceinline__ bool block_needs_mask(int b, int p_first, int S, int window) {
+    return (b * kBlockTokens + kBlockTokens - 1 > p_first) ||
+           (window > 0 && b * kBlockTokens < S - window);
 }
 
 // Global->LDS loads need about sixteen wavefronts per compute unit to reach
@@ -458,7 +579,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     PArgs a, const uint16_t* __restrict__ qg, const uint8_t* __restrict__ kcg,
     const uint8_t* __restrict__ vcg, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
-    const int32_t* __restrict__ unit_start, uint16_t* __restrict__ out,
+    int32_t* __restrict__ unit_start, uint16_t* __restrict__ out,
     float* __restrict__ slot_o, float* __restrict__ slot_lse) {
     constexpr int NT = NW * kWave;
     constexpr int TILE_BYTES = kBlockTokens * D * 2;  // one (block, head) K or V tile
@@ -472,85 +593,32 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     static_assert(CPT * (NS - 2) < 64, "vmcnt range");
 
     __shared__ __attribute__((aligned(16))) uint8_t stage[NS][2 * TILE_BYTES];
-    // Block ids of the loader's request, blocks [wb, wb + 128) at bt_win[b & 127],
-    // refilled 64 at a time ahead of use.
-    __shared__ int32_t bt_win[128];
+    __shared__ int32_t sched[kInlineSchedSeqs + 1];
 
     const int w = blockIdx.x;
-    const int U = unit_start[a.num_seqs];
-    int us, ue;
-    if (a.spb > 0) {
-        us = (int)min((int64_t)U, (int64_t)w * a.spb);
-        ue = (int)min((int64_t)U, (int64_t)us + a.spb);
-    } else {
-        const int n = sharing_wgs(a, U);
-        if (w >= n) return;
-        us = (int)((int64_t)U * w / n);
-        ue = (int)((int64_t)U * (w + 1) / n);
-    }
-    if (us >= ue) return;
-
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wv = tid / kWave;
     const int l16 = lane & 15, lg = lane >> 4;
 
-    // request owning the first unit: the largest i with unit_start[i] <= us
-    Cursor c0;
-    {
-        int lo = 0, hi = a.num_seqs - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (unit_start[mid] <= us) lo = mid; else hi = mid - 1;
+    const int32_t* ustart = unit_start;
+    if (a.inline_sched) {
+        if (wv == 0) {
+            sched_prefix(a, q_start, seq_lens, sched, lane);
+            if (w == 0)
+                for (int i = lane; i <= a.num_seqs; i += kWave) unit_start[i] = sched[i];
         }
-        c0.i = lo;
-        c0.rq = req_geom(a, q_start, seq_lens, lo);
-        const int off = us - unit_start[lo];
-        c0.pq = off / c0.rq.nb;
-        c0.b = c0.rq.b_lo + (off - c0.pq * c0.rq.nb);
+        __syncthreads();
+        ustart = sched;
     }
+    const int U = uniform_load(ustart + a.num_seqs);
+    int us, ue;
+    unit_range(a, U, w, us, ue);
+    if (us >= ue) return;
+    const Cursor c0 = locate_unit(a, q_start, seq_lens, ustart, us);
 
     const uint32_t stage_lds =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)&stage[0][0];
-    const uint32_t bt_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int32_t*)&bt_win[0];
-    int win_req = -1, wb = 0;  // block-id window of the loader (wavefront-uniform)
-    int half_base = -1;        // first block of the 64 ids cached in bt_lane
-    int bt_lane = 0;           // lane j: id of block half_base + j
-    // Entries for blocks [b0, b0 + 64) of request req (b0 a multiple of 64),
-    // loaded by wavefront 0; indices past the table row are clamped (never used).
-    auto bt_refill = [&](int req, int b0) {
-        if (wv == 0) {
-            const int idx = min(b0 + lane, a.max_blocks - 1);
-            dma4(bt_lds + (b0 & 127) * 4, block_tables + (int64_t)req * a.max_blocks + idx);
-        }
-    };
-    // Physical block of the loader's unit.  Inside a pair the loader walks
-    // blocks upwards, so the window only slides forward; a new pair (or
-    // request) restarts it synchronously.
-    auto phys_of = [&](const Cursor& c) -> int {
-        if (c.i != win_req || c.b < wb || c.b >= wb + 128) {
-            win_req = c.i;
-            wb = c.b & ~63;
-            bt_refill(c.i, wb);
-            bt_refill(c.i, wb + 64);
-            if (wv == 0) wait_vmcnt<0>();
-            if constexpr (NW > 1) lds_barrier();
-            half_base = -1;
-        } else if (c.b >= wb + 64) {
-            // blocks [wb, wb + 64) are behind the loader for good: refill their
-            // half with [wb + 128, wb + 192), needed 64 units from now
-            bt_refill(c.i, wb + 128);
-            wb += 64;
-        }
-        // One LDS read per 64 blocks brings the current half into a register;
-        // each block's id is then a readlane away.
-        if ((c.b & ~63) != half_base) {
-            half_base = c.b & ~63;
-            bt_lane = bt_win[(half_base & 127) + lane];
-        }
-        return __builtin_amdgcn_readlane(bt_lane, c.b - half_base);
-    };
-
     // One unit = one block's K and V tiles, copied into an LDS stage with CPT
     // global->LDS loads per thread (wavefront w's c-th load fills the 1 KiB
     // at chunk c*NT + 64w).  Every call issues exactly CPT loads, invalid
@@ -559,9 +627,8 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     // Bit s: stage s holds a valid block.  Every wavefront runs the same
     // loader steps, so each keeps its own copy in a scalar register.
     uint32_t ok_mask = 0;
-    auto dma_unit = [&](const Cursor& c, int st) {
-        const int g = c.rq.rg == 1 ? c.pq : c.pq / c.rq.rg;
-        int phys = phys_of(c);
+    auto dma_unit = [&](const Cursor& c, int st, int phys) {
+        const int g = c.g;
         const bool ok = phys >= 0 && phys < a.num_blocks;
         ok_mask = ok ? (ok_mask | (1u << st)) : (ok_mask & ~(1u << st));
         phys = ok ? phys : 0;
@@ -577,7 +644,8 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     };
 
     // ---- state of the pair being computed
-    int st_i = -1, st_pq = -1, st_g = 0, st_rg = 0;
+    int st_i = -1, st_g = -1, st_rg = -1;
+    int st_ps = 0;  // first unit of the pair
     ReqGeom srq{};
     bool active = false;
     bf16x8_t qop[TPW][KC];
@@ -589,12 +657,13 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     // maximum, neg_m = -m_r (0 while the row has seen no key).
     float m_r[TPW], l_r[TPW], thr[TPW], neg_m[TPW];
 
-    auto init_pair = [&](const Cursor& c) {
+    // Pair of cursor c, reached at unit u.
+    auto init_pair = [&](const Cursor& c, int u) {
         st_i = c.i;
-        st_pq = c.pq;
+        st_ps = u - (c.b - c.rq.b_lo);
         srq = c.rq;
-        st_g = c.pq / c.rq.rg;
-        st_rg = c.pq - st_g * c.rq.rg;
+        st_g = c.g;
+        st_rg = c.r;
         const int rows = a.group * srq.n;
         const int wrow0 = st_rg * ROWS + wv * TPW * 16;
         active = wrow0 < rows;
@@ -627,8 +696,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
 
     auto flush_pair = [&]() {
         if (!active) return;
-        const int ps = unit_start[st_i] + st_pq * srq.nb;
-        const bool whole = ps >= us && ps + srq.nb <= ue;
+        const bool whole = st_ps >= us && st_ps + srq.nb <= ue;
         const int rows = a.group * srq.n;
         const int64_t slot = (int64_t)(st_i * a.hkv + st_g) * a.rg_max + st_rg + w;
 #pragma unroll
@@ -676,55 +744,13 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
                 sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[t][cc], sacc[t], 0, 0, 0);
         }
         const int p_first = srq.S - srq.n;  // position of the request's first query row
-        const int key0 = b * kBlockTokens + 4 * lg;
-        // blocks below the first row's position and inside the last row's
-        // window are fully visible to every row of the request
-        const bool need_mask = (b * kBlockTokens + kBlockTokens - 1 > p_first) ||
-                               (a.window > 0 && b * kBlockTokens < srq.S - a.window);
+        const bool need_mask = block_needs_mask(b, p_first, srq.S, a.window);
         i16x4_t pop[TPW];
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) {
-            float sv[4];  // raw scores <q, k> of keys key0 .. key0 + 3
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sv[r] = sacc[t][r];
-            if (need_mask) {
-                const int p = p_first + row_j[t];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int key = key0 + r;
-                    const bool vis = row_j[t] >= 0 && key <= p && (a.window == 0 || key > p - a.window);
-                    sv[r] = vis ? sv[r] : -INFINITY;
-                }
-            }
-            // The exponentials are taken against the stored maximum m_r as long
-            // as no score exceeds it by more than 2^kSlackLog2; only then (on a
-            // row's first keys, and rarely after) does the wavefront reduce
-            // the new row maximum over the row's four lanes and rescale.  The
-            // weights stay below 2^kSlackLog2, and bf16 rounds them with the
-            // same relative error at any magnitude.
-            const float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-            if (__builtin_amdgcn_ballot_w64(!(mx <= thr[t]))) {
-                const float rmax = row_max_4lanes(mx) * a.scale_log2;
-                if (rmax > m_r[t]) {
-                    // m_r = -inf: nothing accumulated yet, alpha = 0 keeps it 0
-                    const float alpha = __builtin_amdgcn_exp2f(m_r[t] - rmax);
-                    l_r[t] *= alpha;
-#pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
-                    m_r[t] = rmax;
-                    neg_m[t] = -rmax;
-                    thr[t] = (rmax + kSlackLog2) * a.inv_scale_log2;
-                }
-            }
-            // exponent arguments are <= kSlackLog2: the raw v_exp_f32 is exact
-            // enough and results below 2^-126 only flush to zero
-            float pr[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[r], a.scale_log2, neg_m[t]));
-            l_r[t] += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-            pop[t] = __builtin_bit_cast(i16x4_t, make_uint2(pack_bf16x2(pr[0], pr[1]),
-                                                            pack_bf16x2(pr[2], pr[3])));
-        }
+        for (int t = 0; t < TPW; ++t)
+            pop[t] = softmax_step<DT>(sacc[t], need_mask, row_j[t], p_first, b * kBlockTokens + 4 * lg,
+                                      a.window, a.scale_log2, a.inv_scale_log2, m_r[t], l_r[t],
+                                      thr[t], neg_m[t], o[t]);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             const uint2 vv = *reinterpret_cast<const uint2*>(vs + (dt * 16 + l16) * 32 + lg * 8);
@@ -743,28 +769,35 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     // it again instead of issuing nothing, keeping the count fixed.
     Cursor lc = c0;
     int lu = us;
-    auto dma_next = [&](int st) {
-        dma_unit(lc, st);
+    // Block id of the loader's unit: a scalar load, issued once the previous
+    // unit's compute has read its LDS operands (so that no LDS wait there
+    // also waits for it) and consumed after the next barrier.
+    auto fetch_phys = [&]() { return block_tables[(int64_t)lc.i * a.max_blocks + lc.b]; };
+    auto dma_next = [&](int st, int phys) {
+        dma_unit(lc, st, phys);
         if (lu + 1 < ue) {
             advance(a, q_start, seq_lens, lc);
             ++lu;
         }
     };
 #pragma unroll
-    for (int r = 0; r < PD; ++r) dma_next(r);
+    for (int r = 0; r < PD; ++r) dma_next(r, fetch_phys());
+    int phys_next = fetch_phys();
 
     Cursor cc = c0;
-    init_pair(cc);
+    init_pair(cc, us);
     int st = 0;
     for (int uu = us; uu < ue; ++uu) {
         wait_vmcnt<CPT * (PD - 1)>();
         lds_barrier();
-        dma_next(st == 0 ? NS - 1 : st - 1);
-        if (cc.i != st_i || cc.pq != st_pq) {
+        dma_next(st == 0 ? NS - 1 : st - 1, phys_next);
+        if (cc.i != st_i || cc.g != st_g || cc.r != st_rg) {
             flush_pair();
-            init_pair(cc);
+            init_pair(cc, uu);
         }
         compute(st, cc.b);
+        asm volatile("" ::: "memory");
+        phys_next = fetch_phys();
         advance(a, q_start, seq_lens, cc);
         st = st == NS - 1 ? 0 : st + 1;
     }
@@ -778,6 +811,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
 // chunks); a thread owns one row and four consecutive output dimensions, so
 // all of a thread's slot reads are independent and issued together.
 constexpr int kCombineThreads = 256;
+constexpr int kCombineBatch = 4;
 
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
@@ -810,19 +844,36 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
     const int d0 = (threadIdx.x % QUADS) * 4;
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     if (!empty) {
+        // Slots are read in batches of kCombineBatch with every load of a
+        // batch issued before any is used; a slot past the pair's last
+        // workgroup reads as empty (log-sum-exp -inf).
         const int64_t slot0 = (int64_t)P + wf;
         const int ns = wl - wf + 1;
         float M = -INFINITY;
-        for (int s = 0; s < ns; ++s) M = fmaxf(M, slot_lse[(slot0 + s) * ROWS + lr]);
+        for (int s0 = 0; s0 < ns; s0 += kCombineBatch) {
+#pragma unroll
+            for (int k = 0; k < kCombineBatch; ++k)
+                if (s0 + k < ns) M = fmaxf(M, slot_lse[(slot0 + s0 + k) * ROWS + lr]);
+        }
         if (M != -INFINITY) {
             float L = 0.f;
-            for (int s = 0; s < ns; ++s) {
-                const int64_t srow = (slot0 + s) * ROWS + lr;
-                const float lse = slot_lse[srow];
-                const f32x4_t o = *reinterpret_cast<const f32x4_t*>(slot_o + srow * D + d0);
-                const float f = lse == -INFINITY ? 0.f : exp2f(lse - M);
-                L += f;
-                acc += f * o;
+            for (int s0 = 0; s0 < ns; s0 += kCombineBatch) {
+                float lse[kCombineBatch];
+                f32x4_t o[kCombineBatch];
+#pragma unroll
+                for (int k = 0; k < kCombineBatch; ++k) {
+                    const int64_t srow = (slot0 + s0 + k) * ROWS + lr;
+                    const bool in = s0 + k < ns;
+                    lse[k] = in ? slot_lse[srow] : -INFINITY;
+                    o[k] = in ? *reinterpret_cast<const f32x4_t*>(slot_o + srow * D + d0)
+                              : f32x4_t{0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+                for (int k = 0; k < kCombineBatch; ++k) {
+                    const float f = lse[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(lse[k] - M);
+                    L += f;
+                    acc += f * o[k];
+                }
             }
             acc *= 1.f / L;
         }
@@ -936,6 +987,11 @@ bool with_shape(int d, int nw, int tpw, F&& f) {
     return false;
 }
 
+template <typename S>
+constexpr auto persist_kernel() {
+    return attn_persist<S::D, S::NW, S::TPW, S::PD>;
+}
+
 int validate(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
              int32_t max_seq_len) {
     if (!p) return VERIFY_EINVAL;
@@ -974,8 +1030,9 @@ int resident_wgs() {
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 2; }
     int v = cache[dev].load(std::memory_order_relaxed);
     if (v > 0) return v;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, attn_persist<S::D, S::NW, S::TPW, S::PD>,
-                                                     S::NW * kWave, 0) != hipSuccess || v <= 0) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, persist_kernel<S>(), S::NW * kWave, 0) !=
+            hipSuccess ||
+        v <= 0) {
         (void)hipGetLastError();
         v = 1;
     }
@@ -1062,13 +1119,14 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
 // merge of partial slots.  Returns false if the plan names no known shape.
 bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, int head_dim,
                     hipStream_t stream) {
-    hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
-                       m.unit_start);
+    if (!a.inline_sched)
+        hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
+                           m.unit_start);
     return with_shape(head_dim, pl.nw, pl.tpw, [&](auto sh) {
         using S = decltype(sh);
-        hipLaunchKernelGGL((attn_persist<S::D, S::NW, S::TPW, S::PD>), dim3(a.nwg), dim3(S::NW * kWave), 0,
-                           stream, a, m.q, m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start,
-                           m.unit_start, m.out, m.slot_o, m.slot_lse);
+        hipLaunchKernelGGL(persist_kernel<S>(), dim3(a.nwg), dim3(S::NW * kWave), 0, stream, a, m.q,
+                           m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start, m.unit_start, m.out,
+                           m.slot_o, m.slot_lse);
         const int64_t pairs = (int64_t)a.num_seqs * a.hkv * a.rg_max;
         constexpr int RPB = kCombineThreads / (S::D / 4);
         const unsigned chunks = (unsigned)((a.rows_per_group + RPB - 1) / RPB);
@@ -1157,6 +1215,7 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         a.rg_max = pl.rg_max;
         a.nwg = pl.nwg;
         a.spb = pl.spb;
+        a.inline_sched = p.num_seqs <= kInlineSchedSeqs;
         if (!launch_persist(a, m, pl, p.head_dim, stream)) return VERIFY_EUNSUPPORTED;
         return check_launch();
     }
