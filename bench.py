@@ -7,8 +7,9 @@ verify_accept (vocabulary argmax + greedy acceptance) over one batch of
 synthetic inputs already resident in HBM.  Prints one JSON line:
 
   value         verified tokens/s = sum_i (accept_len_i + 1) / step time
-  roofline      the attention kernel(s): algorithmic bytes per launch / mean
-                launch time (HIP events on the launch stream) vs 8 TB/s HBM
+  roofline      the attention call: algorithmic bytes per launch / mean launch
+                time (HIP events on the launch stream around each call, in a
+                loop of their own after the timed steps) vs 8 TB/s HBM
   cpu_baseline  the CPU oracle on a bounded sample of the same step (first
                 requests of the batch, all their heads and logits rows)
 """
@@ -202,6 +203,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--graph", action=argparse.BooleanOptionalAction, default=False,
+                    help="replay the step as one captured HIP graph instead of launching its "
+                         "kernels one by one (measured slower on this step)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run one plain elementwise kernel that reads "
                          "and writes %d MiB (scale for the HBM byte counters)" % (CALIB_BYTES >> 20))
@@ -254,36 +258,52 @@ def main():
                             bt.t_q_start, max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len,
                             sliding_window=l.window, out=outs[li], workspace=ws[li])
 
-    def step(evs=None):
+    def step():
         for li in range(len(bt.layers)):
-            if evs is not None:
-                evs[li][0].record(stream)
             attention(li)
-            if evs is not None:
-                evs[li][1].record(stream)
         av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start, argmax_out=am, accept_len=acc,
                          num_emitted=ne, emitted=em, workspace=aws)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    run_step = step
+    if args.graph:
+        # The step's launches, captured once: a serving loop replays them
+        # without per-kernel launch work on the host.
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        graph.replay()
+        torch.cuda.synchronize()
+        run_step = graph.replay
 
+    # timed region: K whole steps, no events inside
     K = args.steps
-    attn_ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-                for _ in bt.layers] for _ in range(K)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record(stream)
     for k in range(K):
-        step(attn_ev[k])
+        run_step()
     t1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_step = t0.elapsed_time(t1) / K
-    attn_ms = [float(np.mean([attn_ev[k][li][0].elapsed_time(attn_ev[k][li][1]) for k in range(K)]))
-               for li in range(len(bt.layers))]
+
+    # per-launch time of each attention call (roofline): events on the launch
+    # stream around each call, K calls per layer, after the timed region
+    attn_ms = []
+    for li in range(len(bt.layers)):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(K)]
+        for e0, e1 in evs:
+            e0.record(stream)
+            attention(li)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        attn_ms.append(float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs])))
 
     emitted = int(ne.sum().item())
     proposed = int(bt.num_drafts.sum())
@@ -294,8 +314,8 @@ def main():
     dom = int(np.argmax(abytes))
     achieved = abytes[dom] / (attn_ms[dom] * 1e-3) / 1e9
     step_bytes = sum(abytes) + accept_bytes(bt)
-    log("step %.3f ms (wall %.3f ms), attention %s ms, accept+rest %.3f ms" % (
-        ms_step, wall / K * 1e3, ["%.3f" % x for x in attn_ms], ms_step - sum(attn_ms)))
+    log("step %.3f ms (wall %.3f ms); attention calls timed alone %s ms" % (
+        ms_step, wall / K * 1e3, ["%.3f" % x for x in attn_ms]))
     log("step algorithmic bytes %.3f GB -> %.0f GB/s (%.1f%% of HBM peak); attention layer %d: "
         "%.3f GB in %.3f ms = %.0f GB/s" % (step_bytes / 1e9, step_bytes / ms_step / 1e6,
                                             100 * step_bytes / ms_step / 1e6 / HBM_PEAK_GBS, dom,
@@ -339,7 +359,7 @@ def main():
                    "total_q": T, "mean_context": float(bt.context_len.mean()),
                    "num_q_heads": cfg.num_q_heads, "num_kv_heads": cfg.num_kv_heads,
                    "head_dim": cfg.head_dim, "vocab": cfg.vocab, "layers": len(bt.layers),
-                   "seed": args.seed},
+                   "seed": args.seed, "hip_graph": bool(args.graph)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "algorithmic_bytes": abytes[dom],
