@@ -363,8 +363,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "algorithmic_bytes": abytes[dom],
-                     "kernel": "verify_attention call (attn_schedule + attn_persist + "
-                               "attn_combine_slots), layer %d" % dom},
+                     "kernel": "verify_attention call (attn_persist + attn_combine_slots), "
+                               "layer %d" % dom},
         "step_hbm_frac": step_bytes / ms_step / 1e6 / HBM_PEAK_GBS,
         "scored_positions_per_s": T / (ms_step * 1e-3),
         "rejection_rate": 1 - accepted / max(1, proposed),
