@@ -14,6 +14,8 @@ Functions (each restates the paper's definition; see ``oracle.c``):
   argmax(...)     -- lowest index of the row maximum, plus the top-2 gap.
   accept(...)     -- greedy acceptance: longest matching draft prefix plus one
                      bonus token; rejection rate = rejected / proposed (Sec. 3.1).
+  budget(...)     -- redundancy-aware draft budget (Sec. 4.2, Alg. 2) and the
+                     verify-step descriptor built from the draft lengths.
 """
 from __future__ import annotations
 
@@ -60,6 +62,9 @@ def _load():
     lib.oracle_argmax.restype = ctypes.c_int
     lib.oracle_accept.argtypes = [i32, vp, vp, vp, vp, vp, vp]
     lib.oracle_accept.restype = ctypes.c_int
+    lib.oracle_budget.argtypes = [i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp, vp,
+                                  vp]
+    lib.oracle_budget.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -148,6 +153,40 @@ def accept(q_start, tokens, argmax_rows):
     em = np.zeros(tok.shape[0], dtype=np.int32)
     lib.oracle_accept(num_seqs, _ptr(qs), _ptr(tok), _ptr(am), _ptr(acc), _ptr(ne), _ptr(em))
     return acc, ne, em
+
+
+def budget(cand_start, cand_len, cand_tokens, last_token, alpha: float, g_min: float,
+           ctx_len=None):
+    """Draft lengths of the next verify step (see oracle_budget in oracle.c).
+
+    cand_tokens is [C, max_len]; returns a dict of numpy arrays: score,
+    agree, prefix_len, source, draft_len, q_start, tokens (and seq_lens when
+    ctx_len is given)."""
+    lib = _load()
+    cs = np.ascontiguousarray(cand_start, dtype=np.int32)
+    cl = np.ascontiguousarray(cand_len, dtype=np.int32)
+    ct = np.ascontiguousarray(cand_tokens, dtype=np.int32)
+    if ct.ndim != 2:
+        raise ValueError("cand_tokens must be [candidates, max_len]")
+    lt = np.ascontiguousarray(last_token, dtype=np.int32)
+    B = cs.shape[0] - 1
+    max_len = ct.shape[1]
+    cx = None if ctx_len is None else np.ascontiguousarray(ctx_len, dtype=np.int32)
+    out = dict(score=np.zeros(B, np.float64), agree=np.zeros(B, np.int32),
+               prefix_len=np.zeros(B, np.int32), source=np.zeros(B, np.int32),
+               draft_len=np.zeros(B, np.int32), q_start=np.zeros(B + 1, np.int32),
+               tokens=np.zeros(B * (max_len + 1), np.int32))
+    if cx is not None:
+        out["seq_lens"] = np.zeros(B, np.int32)
+    rc = lib.oracle_budget(B, max_len, _ptr(cs), _ptr(cl), _ptr(ct), _ptr(lt),
+                           _ptr(cx) if cx is not None else None, float(alpha), float(g_min),
+                           _ptr(out["score"]), _ptr(out["agree"]), _ptr(out["prefix_len"]),
+                           _ptr(out["source"]), _ptr(out["draft_len"]), _ptr(out["q_start"]),
+                           _ptr(out["tokens"]), _ptr(out["seq_lens"]) if cx is not None else None)
+    if rc != 0:
+        raise ValueError("oracle_budget rejected its arguments")
+    out["tokens"] = out["tokens"][: out["q_start"][-1]]
+    return out
 
 
 def rejection_rate(accept_len, q_start):

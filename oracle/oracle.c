@@ -20,6 +20,9 @@
  *                        (plus the gap to the runner-up, for near-tie flags).
  *   oracle_accept     -- greedy acceptance: the longest prefix of drafts equal
  *                        to the target's argmax, followed by one bonus token.
+ *   oracle_budget     -- redundancy-aware draft budget (Sec. 4.2, Alg. 2): the
+ *                        per-request draft lengths and the verify step's
+ *                        batch descriptor built from them.
  *
  * Readings of the paper that this file encodes (the paper relies on its
  * serving engine for verification and does not spell these out):
@@ -204,6 +207,116 @@ int oracle_accept(int32_t num_seqs, const int32_t *q_start, const int32_t *token
             emitted[q0 + j] = j < m ? tokens[q0 + j + 1] : (j == m ? argmax[q0 + m] : -1);
         accept_len[i] = m;
         num_emitted[i] = m + 1;
+    }
+    return 0;
+}
+
+/*
+ * Redundancy-aware budget allocation (Sec. 4.2 and its pseudocode, Alg. 2):
+ * the per-request draft lengths L_i of the next verify step, and the verify
+ * step's batch descriptor built from them.
+ *
+ * Inputs.  Request i owns candidate continuations cand_start[i] ..
+ * cand_start[i+1]-1, rows of cand_tokens [C][max_len] with cand_len[r] valid
+ * tokens each; last_token[i] is its last committed token; ctx_len (nullable)
+ * its cached context length.  alpha and g_min are the method's two
+ * hyperparameters.
+ *
+ * Readings of the paper (it leaves these open):
+ *   - n_i counts every candidate of the request, empty ones included;
+ *   - the most frequent continuation prefix CT_i* is the non-empty prefix that
+ *     the most candidates start with; among equally frequent ones the longest,
+ *     then the lexicographically smallest; c_i is the number of candidates
+ *     starting with it (0, and g_i = 0, when every candidate is empty);
+ *   - p(n) = g_min + (1 - g_min)(1 - e^(1-n)): the equation's form, the one
+ *     that gives p(1) = g_min, the minimum confidence under the least support
+ *     (the pseudocode's exponent -n does not);
+ *   - B_t = floor(alpha / bz) with bz = num_seqs; G = sum_i g_i in ascending i;
+ *   - L_i = max(|CT_i*|, floor((B_t * g_i) / G)), the share being 0 when G = 0,
+ *     and at most the length of the longest candidate starting with CT_i*
+ *     (the lowest row among equals): its first L_i tokens are the drafts.
+ *
+ * Outputs: score g_i, agree c_i, prefix_len |CT_i*|, source (that candidate's
+ * row, -1 if none), draft_len L_i; q_start[num_seqs+1] (exclusive prefix sum
+ * of L_i + 1), tokens (per request: last_token, then the L_i drafts) and, if
+ * ctx_len is given, seq_lens = ctx_len + L_i + 1.
+ */
+static int common_prefix(const int32_t *a, int32_t la, const int32_t *b, int32_t lb)
+{
+    int32_t m = la < lb ? la : lb, k = 0;
+    while (k < m && a[k] == b[k]) ++k;
+    return k;
+}
+
+int oracle_budget(int32_t num_seqs, int32_t max_len, const int32_t *cand_start,
+                  const int32_t *cand_len, const int32_t *cand_tokens,
+                  const int32_t *last_token, const int32_t *ctx_len, double alpha,
+                  double g_min, double *score, int32_t *agree, int32_t *prefix_len,
+                  int32_t *source, int32_t *draft_len, int32_t *q_start, int32_t *tokens,
+                  int32_t *seq_lens)
+{
+    if (num_seqs < 0 || max_len < 0 || !(alpha >= 0.0) || !(g_min >= 0.0 && g_min <= 1.0))
+        return -1;
+    q_start[0] = 0;
+    if (num_seqs == 0) return 0;
+    const double bt = floor(alpha / (double)num_seqs);
+    double G = 0.0;
+    for (int i = 0; i < num_seqs; ++i) {
+        const int32_t r0 = cand_start[i], n = cand_start[i + 1] - r0;
+        score[i] = 0.0; agree[i] = 0; prefix_len[i] = 0; source[i] = -1;
+        /* The prefixes starting with one first token are all shared by at most
+         * the candidates of that first token; the group's longest common prefix
+         * is shared by all of them.  So the most frequent prefix is the longest
+         * common prefix of the largest first-token group. */
+        int32_t best_c = 0, best_l = 0, best_tok = 0, best_row = -1;
+        for (int32_t a = 0; a < n; ++a) {
+            const int32_t ra = r0 + a;
+            if (cand_len[ra] <= 0) continue;
+            const int32_t *ta = cand_tokens + (int64_t)ra * max_len;
+            int32_t c = 0, l = cand_len[ra];
+            for (int32_t b = 0; b < n; ++b) {
+                const int32_t rb = r0 + b;
+                if (cand_len[rb] <= 0) continue;
+                const int32_t *tb = cand_tokens + (int64_t)rb * max_len;
+                if (tb[0] != ta[0]) continue;
+                ++c;
+                const int k = common_prefix(ta, cand_len[ra], tb, cand_len[rb]);
+                if (k < l) l = k;
+            }
+            if (c > best_c || (c == best_c && (l > best_l || (l == best_l && ta[0] < best_tok)))) {
+                best_c = c; best_l = l; best_tok = ta[0]; best_row = ra;
+            }
+        }
+        if (best_c == 0) continue;
+        /* drafts come from the longest candidate of the group (lowest row on ties) */
+        int32_t src = -1;
+        for (int32_t b = 0; b < n; ++b) {
+            const int32_t rb = r0 + b;
+            if (cand_len[rb] <= 0 || cand_tokens[(int64_t)rb * max_len] != best_tok) continue;
+            if (src < 0 || cand_len[rb] > cand_len[src]) src = rb;
+        }
+        (void)best_row;
+        const double p = g_min + (1.0 - g_min) * (1.0 - exp(1.0 - (double)n));
+        score[i] = ((double)best_c / (double)n) * p;
+        agree[i] = best_c;
+        prefix_len[i] = best_l;
+        source[i] = src;
+    }
+    for (int i = 0; i < num_seqs; ++i) G += score[i];
+    for (int i = 0; i < num_seqs; ++i) {
+        int64_t L = 0;
+        if (source[i] >= 0) {
+            const double share = G > 0.0 ? floor((bt * score[i]) / G) : 0.0;
+            L = prefix_len[i];
+            if (share > (double)L) L = (int64_t)share;
+            if (L > cand_len[source[i]]) L = cand_len[source[i]];
+        }
+        draft_len[i] = (int32_t)L;
+        q_start[i + 1] = q_start[i] + (int32_t)L + 1;
+        tokens[q_start[i]] = last_token[i];
+        for (int64_t j = 0; j < L; ++j)
+            tokens[q_start[i] + 1 + j] = cand_tokens[(int64_t)source[i] * max_len + j];
+        if (ctx_len) seq_lens[i] = ctx_len[i] + (int32_t)L + 1;
     }
     return 0;
 }
