@@ -143,6 +143,52 @@ def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
     print("\n".join(lines))
 
 
+def budget_timing(av, workload, *, oracle_ok: bool, batch: int, steps: int, dev: str):
+    """Mean device time of one verify_budget call (Sec. 4.2, Alg. 2) on seeded
+    candidate sets for the batch, and the oracle's time for the same call.  The
+    call is latency-bound (one small launch), so it has no roofline."""
+    import numpy as np
+    import torch
+    start, lens, toks = workload.draw_candidates(1, batch)
+    rng = np.random.default_rng(2)
+    last = rng.integers(0, 151936, size=batch).astype(np.int32)
+    ctx = rng.integers(2048, 16385, size=batch).astype(np.int32)
+    d = lambda a: torch.as_tensor(a, device=dev)
+    args = (d(start), d(lens), d(toks), d(last))
+    ctx_d = d(ctx)
+    # B_t = floor(alpha / bz) is the whole batch's budget: eight drafts per
+    # request on average, as in the verify workload
+    alpha = 8.0 * batch * batch
+    out = av.verify_budget(*args, alpha=alpha, g_min=0.3, ctx_len=ctx_d)
+    # A call is far shorter than its host-side launch, so the calls are captured
+    # back to back in one HIP graph and the replay is timed: device time only.
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(steps):
+            av.verify_budget(*args, alpha=alpha, g_min=0.3, ctx_len=ctx_d, out=out)
+    graph.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    res = {"us": e0.elapsed_time(e1) * 1e3 / steps, "batch": batch,
+           "candidates": int(start[-1]), "max_len": int(toks.shape[1]), "alpha": alpha, "g_min": 0.3,
+           "mean_draft_len": float(out["draft_len"].float().mean().item())}
+    if oracle_ok:
+        import oracle
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 0.5:
+            oracle.budget(start, lens, toks, last, alpha, 0.3, ctx_len=ctx)
+            reps += 1
+        res["oracle_us"] = (time.perf_counter() - t0) / reps * 1e6
+    return res
+
+
 def cpu_baseline(bt, budget_s: float):
     """Time the oracle (as it stands) on the same step: request by request, all
     heads, every layer, and the request's logits rows, until the whole batch is
@@ -331,6 +377,9 @@ def main():
         torch.cuda.synchronize()
         del x, y
 
+    budget = budget_timing(av, workload, oracle_ok=args.cpu_budget > 0, batch=B, steps=K, dev=dev)
+    log("budget allocation (verify_budget):", budget)
+
     traffic = stored_traffic(cfg.name)
     if traffic is not None:
         log("HBM traffic per attention call (counters): %.4f GB vs algorithmic %.4f GB" % (
@@ -369,6 +418,7 @@ def main():
         "scored_positions_per_s": T / (ms_step * 1e-3),
         "rejection_rate": 1 - accepted / max(1, proposed),
         "cpu_baseline": cpu,
+        "budget_alloc": budget,
     }
     print(json.dumps(res), flush=True)
 

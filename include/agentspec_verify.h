@@ -17,6 +17,9 @@
  *                       greedy acceptance: the longest draft prefix that agrees
  *                       with the target, plus one bonus token.  The rejection
  *                       rate of Sec. 3.1 is (k_i - accept_len_i) / k_i.
+ *   verify_budget    -- the step upstream of both: the redundancy-aware draft
+ *                       lengths k_i = L_i of Sec. 4.2 / Alg. 2, and the verify
+ *                       step's q_start / tokens / seq_lens built from them.
  *
  * Conventions shared by both calls
  * --------------------------------
@@ -146,6 +149,51 @@ int verify_accept(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_
                   const int32_t *q_start, int32_t *argmax_out, int32_t *accept_len,
                   int32_t *num_emitted, int32_t *emitted, void *workspace,
                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * verify_budget -- redundancy-aware draft budget (Sec. 4.2, Alg. 2).
+ *
+ * Request i owns the candidate continuations retrieved for it (rows
+ * cand_start[i] .. cand_start[i+1]-1; the paper retrieves them from the
+ * request's generation history under the same semantic block and query).
+ * The call scores each request's consensus and hands out the batch budget:
+ *
+ *   n_i   = number of candidates of request i (empty ones included)
+ *   CT_i* = the non-empty prefix that the most candidates start with (the
+ *           longest, then the lexicographically smallest, among equally
+ *           frequent ones); c_i = the number of candidates starting with it
+ *   p(n)  = g_min + (1 - g_min) (1 - e^(1-n))
+ *   g_i   = (c_i / n_i) p(n_i)            (0 if request i has no non-empty one)
+ *   B_t   = floor(alpha / num_seqs),  G = sum_i g_i (ascending i, double)
+ *   L_i   = max(|CT_i*|, floor(B_t g_i / G)) (share 0 if G = 0), at most the
+ *           length of the longest candidate starting with CT_i* (the lowest row
+ *           among equals), whose first L_i tokens become request i's drafts.
+ *
+ *   cand_start  [num_seqs + 1] int32, non-decreasing, cand_start[num_seqs] <= num_cands
+ *               (device values outside [0, num_cands] are clamped)
+ *   cand_len    [num_cands] int32, tokens per candidate, clamped to [0, max_cand_len]
+ *   cand_tokens [num_cands][max_cand_len] int32, row-major
+ *   last_token  [num_seqs] int32: request i's last committed token
+ *   ctx_len     [num_seqs] int32 or NULL: cached context length L_ctx of request i
+ *   alpha >= 0, 0 <= g_min <= 1 (host doubles)
+ * Outputs (device, caller-owned):
+ *   score [num_seqs] double g_i; agree, prefix_len, source, draft_len
+ *   [num_seqs] int32 (c_i, |CT_i*|, candidate row or -1, L_i);
+ *   q_start [num_seqs + 1] int32: exclusive prefix sum of L_i + 1;
+ *   tokens  [tokens_capacity] int32, capacity >= num_seqs * (max_cand_len + 1):
+ *           tokens[q_start[i]] = last_token[i], then the L_i drafts;
+ *   seq_lens [num_seqs] int32, given iff ctx_len is: ctx_len[i] + L_i + 1.
+ * q_start, tokens and seq_lens are the verify_attention / verify_accept
+ * descriptor of the next step (max_q_len <= max_cand_len + 1 bounds it).
+ * No workspace; VERIFY_EINVAL on null or inconsistent arguments,
+ * VERIFY_EUNSUPPORTED if num_seqs * (max_cand_len + 1) >= 2^31.
+ */
+int verify_budget(int32_t num_seqs, int32_t num_cands, int32_t max_cand_len,
+                  const int32_t *cand_start, const int32_t *cand_len, const int32_t *cand_tokens,
+                  const int32_t *last_token, const int32_t *ctx_len, double alpha, double g_min,
+                  double *score, int32_t *agree, int32_t *prefix_len, int32_t *source,
+                  int32_t *draft_len, int32_t *q_start, int32_t *tokens, int64_t tokens_capacity,
+                  int32_t *seq_lens, hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char *verify_status_string(int status);

@@ -68,6 +68,10 @@ def library(path: Optional[str] = None):
     lib.verify_accept_workspace_size.restype = ctypes.c_int
     lib.verify_accept.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.verify_accept.restype = ctypes.c_int
+    f64 = ctypes.c_double
+    lib.verify_budget.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp,
+                                  vp, i64, vp, vp]
+    lib.verify_budget.restype = ctypes.c_int
     lib.verify_status_string.argtypes = [ctypes.c_int]
     lib.verify_status_string.restype = ctypes.c_char_p
     lib.verify_abi_version.argtypes = []
@@ -220,3 +224,40 @@ def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, 
         _stream_ptr(stream, dev))
     _check(rc, "verify_accept")
     return accept_len, num_emitted, emitted, argmax_out
+
+
+def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float, g_min: float,
+                  ctx_len=None, out=None, stream=None):
+    """Redundancy-aware draft lengths (Sec. 4.2, Alg. 2) and the next verify
+    step's descriptor.
+
+    cand_start [B+1], cand_len [C], cand_tokens [C, max_len], last_token [B]
+    and ctx_len [B] (optional) are int32 device tensors.  Returns a dict of
+    device tensors: score (float64), agree, prefix_len, source, draft_len,
+    q_start, tokens (capacity B * (max_len + 1); q_start[-1] entries used) and,
+    with ctx_len, seq_lens.  ``out`` may hold preallocated tensors by name.
+    """
+    import torch
+    B = cand_start.shape[0] - 1
+    C, max_len = cand_tokens.shape
+    dev = cand_start.device
+    i32 = torch.int32
+    o = dict(out or {})
+    shapes = dict(score=(B, torch.float64), agree=(B, i32), prefix_len=(B, i32), source=(B, i32),
+                  draft_len=(B, i32), q_start=(B + 1, i32), tokens=(B * (max_len + 1), i32))
+    if ctx_len is not None:
+        shapes["seq_lens"] = (B, i32)
+    for k, (n, dt) in shapes.items():
+        if k not in o:
+            o[k] = torch.empty(max(n, 1) if k == "tokens" else n, dtype=dt, device=dev)
+    rc = library().verify_budget(
+        B, C, max_len, _dev_ptr(cand_start, "cand_start", i32), _dev_ptr(cand_len, "cand_len", i32),
+        _dev_ptr(cand_tokens, "cand_tokens", i32), _dev_ptr(last_token, "last_token", i32),
+        _dev_ptr(ctx_len, "ctx_len", i32), float(alpha), float(g_min),
+        _dev_ptr(o["score"], "score", torch.float64), _dev_ptr(o["agree"], "agree", i32),
+        _dev_ptr(o["prefix_len"], "prefix_len", i32), _dev_ptr(o["source"], "source", i32),
+        _dev_ptr(o["draft_len"], "draft_len", i32), _dev_ptr(o["q_start"], "q_start", i32),
+        _dev_ptr(o["tokens"], "tokens", i32), o["tokens"].numel(),
+        _dev_ptr(o.get("seq_lens"), "seq_lens", i32), _stream_ptr(stream, dev))
+    _check(rc, "verify_budget")
+    return o

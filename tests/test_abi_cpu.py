@@ -140,3 +140,33 @@ def test_accept_argument_validation():
     assert lib.verify_accept(4, 40, 100, 0, av.F32, *args, dummy, n.value - 1, None) == av.EWORKSPACE
     # empty batch is a no-op
     assert lib.verify_accept(0, 0, 100, 0, av.F32, *([None] * 8), 0, None) == 0
+
+
+def test_budget_argument_validation():
+    lib = av.library()
+    d = ctypes.c_void_p(0x1000)
+    ok = dict(num_seqs=4, num_cands=10, max_len=8, cs=d, cl=d, ct=d, lt=d, cx=None, alpha=10.0,
+              g_min=0.5, score=d, agree=d, prefix=d, source=d, dl=d, qs=d, tok=d, cap=4 * 9, sl=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return lib.verify_budget(a["num_seqs"], a["num_cands"], a["max_len"], a["cs"], a["cl"], a["ct"],
+                                 a["lt"], a["cx"], a["alpha"], a["g_min"], a["score"], a["agree"],
+                                 a["prefix"], a["source"], a["dl"], a["qs"], a["tok"], a["cap"], a["sl"],
+                                 None)
+
+    assert call(num_seqs=-1) == av.EINVAL
+    assert call(num_cands=-1) == av.EINVAL
+    assert call(max_len=0) == av.EINVAL
+    assert call(alpha=-1.0) == av.EINVAL
+    assert call(alpha=float("nan")) == av.EINVAL
+    assert call(g_min=1.5) == av.EINVAL
+    assert call(g_min=-0.1) == av.EINVAL
+    assert call(cap=4 * 9 - 1) == av.EINVAL           # tokens capacity below B * (max_len + 1)
+    assert call(qs=None) == av.EINVAL
+    assert call(source=None) == av.EINVAL
+    assert call(ct=None) == av.EINVAL
+    assert call(cx=d) == av.EINVAL                    # ctx_len without seq_lens
+    assert call(sl=d) == av.EINVAL                    # seq_lens without ctx_len
+    assert call(num_seqs=1 << 20, max_len=4096, cap=1 << 40) == av.EUNSUPPORTED

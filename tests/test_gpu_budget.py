@@ -1,0 +1,145 @@
+"""verify_budget (Sec. 4.2, Alg. 2) on the GPU against the oracle.
+
+Integer outputs must match exactly and scores to a few ulp (both sides work
+in double; the device exp and the host exp may differ in the last bit).  A
+draft length decided by floor(B_t g_i / G) may differ only where the oracle's
+share lies within 1e-9 of an integer; the descriptor is then checked against
+the GPU's choice."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_24004_amd as av
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def random_batch(rng, B, n_max, len_max, vocab_max):
+    reqs = []
+    for _ in range(B):
+        n = int(rng.integers(0, n_max + 1))
+        vocab = int(rng.integers(1, vocab_max + 1))
+        base = list(rng.integers(0, vocab, size=len_max))
+        reqs.append([base[:int(rng.integers(0, len_max // 2 + 1))]
+                     + list(rng.integers(0, vocab, size=int(rng.integers(0, len_max // 2 + 1))))
+                     for _ in range(n)])
+    rows = [c[:len_max] for r in reqs for c in r]
+    start = np.cumsum([0] + [len(r) for r in reqs]).astype(np.int32)
+    lens = np.array([len(c) for c in rows], dtype=np.int32)
+    toks = np.zeros((max(len(rows), 1), len_max), dtype=np.int32)
+    for i, c in enumerate(rows):
+        toks[i, :len(c)] = c
+    if len(rows) == 0:
+        lens = np.zeros(1, dtype=np.int32)
+    return start, lens, toks
+
+
+def check(start, lens, toks, last, ctx, alpha, g_min):
+    d = lambda a: torch.as_tensor(a, device=DEV)
+    got = av.verify_budget(d(start), d(lens), d(toks), d(last), ctx_len=d(ctx), alpha=alpha, g_min=g_min)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in got.items()}
+    ref = oracle.budget(start, lens, toks, last, alpha, g_min, ctx_len=ctx)
+    B = len(last)
+    for k in ("agree", "prefix_len", "source"):
+        np.testing.assert_array_equal(got[k], ref[k], err_msg=k)
+    np.testing.assert_allclose(got["score"], ref["score"], rtol=4e-16 * 8, atol=0, err_msg="score")
+    bt = math.floor(alpha / B) if B else 0
+    G = float(np.sum(ref["score"]))
+    ambiguous = 0
+    for i in range(B):
+        if got["draft_len"][i] == ref["draft_len"][i]:
+            continue
+        x = bt * ref["score"][i] / G
+        assert abs(x - round(x)) < 1e-9 * max(1.0, abs(x)), ("draft_len", i, got["draft_len"][i],
+                                                                ref["draft_len"][i])
+        assert abs(int(got["draft_len"][i]) - int(ref["draft_len"][i])) == 1
+        ambiguous += 1
+    # descriptor from the GPU's draft lengths
+    L = got["draft_len"].astype(np.int64)
+    qs = np.concatenate([[0], np.cumsum(L + 1)]).astype(np.int32)
+    np.testing.assert_array_equal(got["q_start"], qs, err_msg="q_start")
+    exp_tok = []
+    for i in range(B):
+        exp_tok.append(last[i])
+        if L[i]:
+            exp_tok.extend(toks[ref["source"][i], :L[i]].tolist())
+    np.testing.assert_array_equal(got["tokens"][:qs[-1]], np.array(exp_tok, dtype=np.int32), err_msg="tokens")
+    np.testing.assert_array_equal(got["seq_lens"], ctx + L + 1, err_msg="seq_lens")
+    return ambiguous
+
+
+@pytest.mark.parametrize("B,n_max,len_max,vocab_max", [
+    (1, 3, 4, 2), (7, 6, 6, 3), (32, 16, 32, 4), (33, 64, 8, 2), (200, 70, 12, 3), (3000, 12, 32, 5)])
+def test_budget_matches_oracle(B, n_max, len_max, vocab_max):
+    rng = np.random.default_rng(B * 31 + n_max)
+    for trial in range(4):
+        start, lens, toks = random_batch(rng, B, n_max, len_max, vocab_max)
+        last = rng.integers(0, 1000, size=B).astype(np.int32)
+        ctx = rng.integers(0, 5000, size=B).astype(np.int32)
+        alpha = float(rng.choice([0.0, 1.0, 37.0, 500.0, 1e5]))
+        g_min = float(rng.choice([0.0, 0.3, 1.0]))
+        say("budget", B, n_max, len_max, trial, alpha, g_min)
+        check(start, lens, toks, last, ctx, alpha, g_min)
+
+
+def test_budget_ties_and_degenerate():
+    rng = np.random.default_rng(5)
+    # identical requests: every share is the same exact fraction of B_t
+    start = np.array([0, 3, 6, 9, 12, 15], dtype=np.int32)
+    toks = np.tile(np.array([[1, 2, 3, 4, 5, 6], [1, 7, 8, 9, 10, 11], [2, 2, 2, 2, 2, 2]],
+                            dtype=np.int32), (5, 1))
+    lens = np.full(15, 6, dtype=np.int32)
+    for alpha in (0.0, 10.0, 25.0, 26.0, 1000.0):
+        check(start, lens, toks, np.arange(5, dtype=np.int32), np.zeros(5, np.int32), alpha, 0.5)
+    # requests without candidates, empty candidates, a single candidate
+    start = np.array([0, 0, 2, 3], dtype=np.int32)
+    toks = np.array([[4, 4], [0, 0], [9, 8]], dtype=np.int32)
+    lens = np.array([2, 0, 2], dtype=np.int32)
+    check(start, lens, toks, np.array([1, 2, 3], np.int32), np.array([5, 6, 7], np.int32), 12.0, 0.2)
+    # no candidates at all
+    check(np.zeros(4, np.int32), np.zeros(1, np.int32), np.zeros((1, 4), np.int32),
+          np.array([1, 2, 3], np.int32), np.array([0, 0, 0], np.int32), 12.0, 0.2)
+
+
+def test_budget_feeds_the_verify_step():
+    """The descriptor verify_budget writes drives verify_accept directly: with
+    logits whose argmax continues every request's drafts, all drafts are
+    accepted and the bonus token follows."""
+    rng = np.random.default_rng(8)
+    start, lens, toks = random_batch(rng, 16, 6, 10, 3)
+    B = 16
+    d = lambda a: torch.as_tensor(a, device=DEV)
+    last = rng.integers(0, 3, size=B).astype(np.int32)
+    o = av.verify_budget(d(start), d(lens), d(toks), d(last), alpha=100.0, g_min=0.4)
+    qs = o["q_start"]
+    T = int(qs[-1].item())
+    tokens = o["tokens"][:T]
+    V = 64
+    tok_h = tokens.cpu().numpy()
+    qs_h = qs.cpu().numpy()
+    logits = torch.full((T, V), -1.0, dtype=torch.float32)
+    bonus = []
+    for i in range(B):
+        q0, q1 = qs_h[i], qs_h[i + 1]
+        for r in range(q0, q1):
+            nxt = tok_h[r + 1] if r + 1 < q1 else 40 + i % 20   # the row's greedy continuation
+            logits[r, nxt] = 5.0
+        bonus.append(40 + i % 20)
+    acc, ne, em, am = av.verify_accept(logits.to(DEV), tokens, qs)
+    np.testing.assert_array_equal(acc.cpu().numpy(), o["draft_len"].cpu().numpy())
+    np.testing.assert_array_equal(ne.cpu().numpy(), o["draft_len"].cpu().numpy() + 1)
+    em_h = em.cpu().numpy()
+    for i in range(B):
+        assert em_h[qs_h[i + 1] - 1] == bonus[i]

@@ -356,3 +356,39 @@ def host_storage(t) -> np.ndarray:
 def dtype_code(name: str) -> int:
     """Storage dtype code shared by the C ABI and the oracle: 0 = fp32, 1 = bf16."""
     return {"f32": 0, "bf16": 1}[name]
+
+
+def draw_candidates(seed: int, batch: int, max_cands: int = 16, max_len: int = 32,
+                    vocab: int = 151936, agree_vocab: int = 4):
+    """Seeded candidate continuations for the budget allocation (Sec. 4.2), in
+    the CSR layout verify_budget takes: (cand_start [B+1], cand_len [C],
+    cand_tokens [C, max_len]) int32 numpy arrays.
+
+    Request i gets U{0..max_cands} candidates.  Each candidate starts with a
+    U{0..max_len/2}-token prefix of a per-request base continuation whose first
+    token comes from a small set (so that candidates agree in varying numbers,
+    the redundancy the method scores), then continues with uniform tokens up
+    to U{0..max_len} tokens in all.
+    """
+    rng = np.random.default_rng([seed, 0xB0D6E7])
+    starts = [0]
+    rows = []
+    for _ in range(batch):
+        n = int(rng.integers(0, max_cands + 1))
+        base = rng.integers(0, vocab, size=max_len)
+        base[0] = int(rng.integers(0, agree_vocab))
+        for _ in range(n):
+            k = int(rng.integers(0, max_len // 2 + 1))
+            total = int(rng.integers(k, max_len + 1))
+            c = np.concatenate([base[:k], rng.integers(0, vocab, size=total - k)])
+            if total > 0 and k == 0:
+                c[0] = int(rng.integers(0, agree_vocab))
+            rows.append(c)
+        starts.append(len(rows))
+    C = max(1, len(rows))
+    lens = np.zeros(C, dtype=np.int32)
+    toks = np.zeros((C, max_len), dtype=np.int32)
+    for r, c in enumerate(rows):
+        lens[r] = len(c)
+        toks[r, :len(c)] = c
+    return np.array(starts, dtype=np.int32), lens, toks
