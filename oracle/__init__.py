@@ -11,6 +11,7 @@ Functions (each restates the paper's definition; see ``oracle.c``):
   attention(...)  -- softmax attention of selected (row, head) pairs against
                      the paged KV cache (speculative verification scores all
                      k+1 positions in one target pass, Sec. 2.2).
+  kv_append(...)  -- the new tokens' K/V written into their paged-cache slots.
   argmax(...)     -- lowest index of the row maximum, plus the top-2 gap.
   accept(...)     -- greedy acceptance: longest matching draft prefix plus one
                      bonus token; rejection rate = rejected / proposed (Sec. 3.1).
@@ -55,8 +56,10 @@ def _load():
         build(force=True)
     lib = ctypes.CDLL(_LIB)
     i32, i64, f64, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
+    lib.oracle_kv_append.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.oracle_kv_append.restype = ctypes.c_int
     lib.oracle_attention.argtypes = [i32, i32, i32, i32, i32, i32, f64, i32, vp, vp, vp, vp,
-                                     vp, vp, i64, vp, vp, vp]
+                                     vp, vp, i64, vp, vp, vp, vp]
     lib.oracle_attention.restype = ctypes.c_int
     lib.oracle_argmax.argtypes = [i64, i64, i64, i32, vp, vp, vp]
     lib.oracle_argmax.restype = ctypes.c_int
@@ -93,11 +96,13 @@ def num_threads() -> int:
 
 def attention(*, num_q_heads: int, num_kv_heads: int, head_dim: int, sliding_window: int,
               scale: float, dtype: int, q, k_cache, v_cache, block_tables, seq_lens, q_start,
-              rows=None, heads=None) -> np.ndarray:
+              rows=None, heads=None, sinks=None) -> np.ndarray:
     """Attention output (float64) for the given (row, head) pairs.
 
     ``rows``/``heads`` are equal-length int arrays; both None means every pair in
     row-major order, returned with shape [T, Hq, D]; otherwise shape [P, D].
+    ``sinks``: optional [Hq] sink logits (one extra softmax logit per head with
+    a zero value, in the units of the scaled scores).
     """
     lib = _load()
     q = _raw(q, dtype)
@@ -116,15 +121,38 @@ def attention(*, num_q_heads: int, num_kv_heads: int, head_dim: int, sliding_win
     rows = np.ascontiguousarray(rows, dtype=np.int32)
     heads = np.ascontiguousarray(heads, dtype=np.int32)
     out = np.zeros((rows.shape[0], head_dim), dtype=np.float64)
+    sk = None if sinks is None else np.ascontiguousarray(sinks, dtype=np.float64)
+    if sk is not None and sk.shape != (num_q_heads,):
+        raise ValueError("sinks must have one entry per query head")
     rc = lib.oracle_attention(num_seqs, num_q_heads, num_kv_heads, head_dim, bt.shape[1],
                               sliding_window, float(scale), dtype, _ptr(q), _ptr(k_cache),
                               _ptr(v_cache), _ptr(bt), _ptr(sl), _ptr(qs), rows.shape[0],
-                              _ptr(rows), _ptr(heads), _ptr(out))
+                              _ptr(rows), _ptr(heads), _ptr(sk) if sk is not None else None,
+                              _ptr(out))
     if rc != 0:
         raise ValueError("oracle_attention rejected its arguments")
     if full:
         return out.reshape(total_q, num_q_heads, head_dim)
     return out
+
+
+def kv_append(*, num_kv_heads: int, head_dim: int, dtype: int, k_new, v_new, block_tables,
+              seq_lens, q_start, k_cache, v_cache):
+    """Copies of k_cache / v_cache (storage bits) with the new tokens' K/V
+    written into their slots (see oracle_kv_append)."""
+    lib = _load()
+    kn = _raw(k_new, dtype)
+    vn = _raw(v_new, dtype)
+    kc = np.array(_raw(k_cache, dtype), copy=True, order="C")
+    vc = np.array(_raw(v_cache, dtype), copy=True, order="C")
+    bt = np.ascontiguousarray(block_tables, dtype=np.int32)
+    sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    qs = np.ascontiguousarray(q_start, dtype=np.int32)
+    rc = lib.oracle_kv_append(sl.shape[0], num_kv_heads, head_dim, bt.shape[1], kc.shape[0], dtype,
+                              _ptr(kn), _ptr(vn), _ptr(bt), _ptr(sl), _ptr(qs), _ptr(kc), _ptr(vc))
+    if rc != 0:
+        raise ValueError("oracle_kv_append rejected its arguments")
+    return kc, vc
 
 
 def argmax(logits, dtype: int, with_gap: bool = True):

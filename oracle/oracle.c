@@ -16,6 +16,7 @@
  *                        plain definition of causal softmax attention of that
  *                        row against its request's paged KV cache, in double
  *                        precision, keys visited in ascending position order.
+ *   oracle_kv_append  -- the new tokens' K/V written into their cache slots.
  *   oracle_argmax     -- per logits row, the lowest index attaining the maximum
  *                        (plus the gap to the runner-up, for near-tie flags).
  *   oracle_accept     -- greedy acceptance: the longest prefix of drafts equal
@@ -78,6 +79,10 @@ static int find_request(int num_seqs, const int32_t *q_start, int32_t row)
 /*
  * out[pair][d] = sum_t w_t V_t[d] / sum_t w_t,  w_t = exp(s_t - max_u s_u),
  * s_t = scale * <q_row_head, K_t>,  t over the visible keys of the row.
+ * With sinks (one logit per query head, in the units of s_t; NULL for none)
+ * the head's sink joins the softmax as a logit whose value is zero: it adds
+ * exp(sink - max) to the denominator only (the attention sinks of the
+ * GPT-OSS models the paper serves; the paper itself does not describe them).
  * Returns 0, or -1 on an argument that cannot be interpreted.
  */
 int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
@@ -85,7 +90,8 @@ int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads
                      double scale, int32_t dtype, const void *q, const void *k_cache,
                      const void *v_cache, const int32_t *block_tables,
                      const int32_t *seq_lens, const int32_t *q_start, int64_t n_pairs,
-                     const int32_t *pair_row, const int32_t *pair_head, double *out)
+                     const int32_t *pair_row, const int32_t *pair_head, const double *sinks,
+                     double *out)
 {
     const int D = head_dim;
     if (num_q_heads % num_kv_heads != 0) return -1;
@@ -128,7 +134,10 @@ int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads
             s[t - lo] = scale * acc;
             if (s[t - lo] > smax) smax = s[t - lo];
         }
-        double denom = 0.0;
+        /* an attention sink is one more logit in the softmax, with no value */
+        const double sink = sinks ? sinks[h] : -INFINITY;
+        if (sink > smax) smax = sink;
+        double denom = sinks ? exp(sink - smax) : 0.0;
         for (int64_t t = lo; t <= p; ++t) {
             const int64_t b = block_tables[(int64_t)i * max_blocks_per_seq + t / 16];
             const double w = exp(s[t - lo] - smax);
@@ -207,6 +216,44 @@ int oracle_accept(int32_t num_seqs, const int32_t *q_start, const int32_t *token
             emitted[q0 + j] = j < m ? tokens[q0 + j + 1] : (j == m ? argmax[q0 + m] : -1);
         accept_len[i] = m;
         num_emitted[i] = m + 1;
+    }
+    return 0;
+}
+
+/*
+ * KV append: the K and V of the verify step's new tokens go into the paged
+ * cache before attention reads them.  Row j of request i is the token at
+ * position p = S_i - n_i + j; its K/V for KV head g land in slot p % 16 of
+ * physical block block_tables[i][p / 16] (layouts as in oracle_attention).
+ * k_new, v_new: [total_q][num_kv_heads][head_dim] in the cache's dtype.  Rows
+ * whose position is negative or whose block id lies outside [0, num_blocks)
+ * are skipped.  Element bits are copied unchanged.
+ */
+int oracle_kv_append(int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
+                     int32_t max_blocks_per_seq, int32_t num_blocks, int32_t dtype,
+                     const void *k_new, const void *v_new, const int32_t *block_tables,
+                     const int32_t *seq_lens, const int32_t *q_start, void *k_cache,
+                     void *v_cache)
+{
+    const int D = head_dim, e = elem_size(dtype), x = 16 / e;
+    if (D % x != 0) return -1;
+    for (int i = 0; i < num_seqs; ++i) {
+        const int64_t n = q_start[i + 1] - q_start[i];
+        for (int64_t j = 0; j < n; ++j) {
+            const int64_t row = q_start[i] + j;
+            const int64_t p = (int64_t)seq_lens[i] - n + j;
+            if (p < 0 || p / 16 >= max_blocks_per_seq) continue;
+            const int64_t b = block_tables[(int64_t)i * max_blocks_per_seq + p / 16];
+            if (b < 0 || b >= num_blocks) continue;
+            for (int g = 0; g < num_kv_heads; ++g)
+                for (int d = 0; d < D; ++d) {
+                    const int64_t src = (row * num_kv_heads + g) * D + d;
+                    const int64_t kidx = (((b * num_kv_heads + g) * (D / x) + d / x) * 16 + p % 16) * x + d % x;
+                    const int64_t vidx = ((b * num_kv_heads + g) * D + d) * 16 + p % 16;
+                    memcpy((char *)k_cache + kidx * e, (const char *)k_new + src * e, e);
+                    memcpy((char *)v_cache + vidx * e, (const char *)v_new + src * e, e);
+                }
+        }
     }
     return 0;
 }
