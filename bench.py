@@ -120,7 +120,9 @@ def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
         raise SystemExit("no calibration dispatch (run bench.py with --copy-calibration)")
     ff = CALIB_BYTES / (fcal * 1024.0)
     wf = CALIB_BYTES / (wcal * 1024.0)
-    attn = [k for k in fk if k.startswith("attn_")]
+    # the kernels one verify_attention call launches (the append is a separate call)
+    call_kernels = ("attn_schedule", "attn_persist", "attn_combine_slots", "attn_valu", "attn_combine")
+    attn = [k for k in fk if k in call_kernels]
     total = 0.0
     lines = []
     for k in sorted(attn):
@@ -143,6 +145,50 @@ def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
     print("\n".join(lines))
 
 
+def graph_time_us(fn, steps: int) -> float:
+    """Mean device time of fn() (one short call): `steps` calls captured back
+    to back in one HIP graph, the replay timed with events (a call shorter
+    than its host-side launch would otherwise measure the launch)."""
+    import torch
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(steps):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps
+
+
+def kv_append_timing(av, bt, steps: int):
+    """Device time of writing the step's new tokens' K/V ([T, Hkv, D] each)
+    into the first layer's cache (verify_kv_append), and its bytes: the new
+    K/V read once and written once."""
+    import torch
+    cfg = bt.cfg
+    l = bt.layers[0]
+    T = bt.total_q
+    g = torch.Generator(device=l.q.device)
+    g.manual_seed(5)
+    k_new = torch.randn((T, cfg.num_kv_heads, cfg.head_dim), generator=g, device=l.q.device).to(l.q.dtype)
+    v_new = torch.randn_like(k_new)
+    # the cache is modified in place: append into copies of the touched blocks' cache
+    kc, vc = l.k_cache.clone(), l.v_cache.clone()
+    fn = lambda: av.verify_kv_append(k_new, v_new, kc, vc, bt.t_block_tables, bt.t_seq_lens,
+                                     bt.t_q_start)
+    fn()
+    us = graph_time_us(fn, steps)
+    nbytes = 2 * 2 * k_new.numel() * k_new.element_size()
+    del kc, vc
+    return {"us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rows": T}
+
+
 def budget_timing(av, workload, *, oracle_ok: bool, batch: int, steps: int, dev: str):
     """Mean device time of one verify_budget call (Sec. 4.2, Alg. 2) on seeded
     candidate sets for the batch, and the oracle's time for the same call.  The
@@ -160,22 +206,9 @@ def budget_timing(av, workload, *, oracle_ok: bool, batch: int, steps: int, dev:
     # request on average, as in the verify workload
     alpha = 8.0 * batch * batch
     out = av.verify_budget(*args, alpha=alpha, g_min=0.3, ctx_len=ctx_d)
-    # A call is far shorter than its host-side launch, so the calls are captured
-    # back to back in one HIP graph and the replay is timed: device time only.
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for _ in range(steps):
-            av.verify_budget(*args, alpha=alpha, g_min=0.3, ctx_len=ctx_d, out=out)
-    graph.replay()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    graph.replay()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    res = {"us": e0.elapsed_time(e1) * 1e3 / steps, "batch": batch,
+    us = graph_time_us(lambda: av.verify_budget(*args, alpha=alpha, g_min=0.3, ctx_len=ctx_d,
+                                                out=out), steps)
+    res = {"us": us, "batch": batch,
            "candidates": int(start[-1]), "max_len": int(toks.shape[1]), "alpha": alpha, "g_min": 0.3,
            "mean_draft_len": float(out["draft_len"].float().mean().item())}
     if oracle_ok:
@@ -203,7 +236,8 @@ def cpu_baseline(bt, budget_s: float):
     host = []
     for layer in bt.layers:
         host.append(dict(q=workload.host_storage(layer.q), k=workload.host_storage(layer.k_cache),
-                         v=workload.host_storage(layer.v_cache), window=layer.window))
+                         v=workload.host_storage(layer.v_cache), window=layer.window,
+                         sinks=None if layer.sinks is None else layer.sinks.cpu().numpy()))
     logits = workload.host_storage(bt.logits)
     B = len(bt.seq_lens)
     passes = []
@@ -221,7 +255,7 @@ def cpu_baseline(bt, budget_s: float):
                                  head_dim=cfg.head_dim, sliding_window=h["window"], scale=0.0,
                                  dtype=code, q=h["q"], k_cache=h["k"], v_cache=h["v"],
                                  block_tables=bt.block_tables, seq_lens=bt.seq_lens,
-                                 q_start=bt.q_start, rows=rows, heads=heads)
+                                 q_start=bt.q_start, rows=rows, heads=heads, sinks=h["sinks"])
             am, _ = oracle.argmax(logits[q0:q1], code, with_gap=False)
             qs = np.array([0, q1 - q0], dtype=np.int32)
             acc, ne, _ = oracle.accept(qs, bt.tokens[q0:q1], am)
@@ -302,7 +336,7 @@ def main():
         l = bt.layers[li]
         av.verify_attention(l.q, l.k_cache, l.v_cache, bt.t_block_tables, bt.t_seq_lens,
                             bt.t_q_start, max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len,
-                            sliding_window=l.window, out=outs[li], workspace=ws[li])
+                            sliding_window=l.window, sinks=l.sinks, out=outs[li], workspace=ws[li])
 
     def step():
         for li in range(len(bt.layers)):
@@ -379,6 +413,8 @@ def main():
 
     budget = budget_timing(av, workload, oracle_ok=args.cpu_budget > 0, batch=B, steps=K, dev=dev)
     log("budget allocation (verify_budget):", budget)
+    append = kv_append_timing(av, bt, K)
+    log("KV append (verify_kv_append):", append)
 
     traffic = stored_traffic(cfg.name)
     if traffic is not None:
@@ -419,6 +455,7 @@ def main():
         "rejection_rate": 1 - accepted / max(1, proposed),
         "cpu_baseline": cpu,
         "budget_alloc": budget,
+        "kv_append": append,
     }
     print(json.dumps(res), flush=True)
 

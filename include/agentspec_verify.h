@@ -20,6 +20,8 @@
  *   verify_budget    -- the step upstream of both: the redundancy-aware draft
  *                       lengths k_i = L_i of Sec. 4.2 / Alg. 2, and the verify
  *                       step's q_start / tokens / seq_lens built from them.
+ *   verify_kv_append -- the n_i new tokens' K/V written into their cache slots
+ *                       before verify_attention reads them.
  *
  * Conventions shared by both calls
  * --------------------------------
@@ -27,8 +29,9 @@
  *    num_seqs+1 entries, q_start[0] = 0, non-decreasing) belong to request i;
  *    total_q = q_start[num_seqs].  Row j of request i is the model input at
  *    absolute position S_i - n_i + j, where S_i = seq_lens[i] counts the
- *    request's cached keys including the n_i new ones (the caller writes the
- *    new tokens' K/V into the cache before the call).
+ *    request's cached keys including the n_i new ones (their K/V are in the
+ *    cache before verify_attention runs: the caller writes them, or calls
+ *    verify_kv_append first on the same stream).
  *  - All array pointers are device pointers owned by the caller.  The library
  *    allocates nothing, keeps no state between calls, never reads device data
  *    on the host, and is safe to call from several host threads on different
@@ -90,7 +93,10 @@ typedef struct verify_attn_params {
  * g = h / (Hq/Hkv) and the visible keys t in [max(0, p-W+1), p] (W > 0) or
  * [0, p] (W = 0):
  *     out[row][h] = sum_t softmax_t(scale * <q[row][h], K_g[t]>) * V_g[t]
- * where K_g[t], V_g[t] are read through block_tables[i][t / 16].
+ * where K_g[t], V_g[t] are read through block_tables[i][t / 16].  With sinks,
+ * head h's sink logit sinks[h] joins each of its rows' softmax as one more
+ * logit whose value is zero (it only enlarges the denominator): the attention
+ * sinks of GPT-OSS models, which the paper serves but does not describe.
  *
  *   q            [total_q][Hq][D]                     (dtype)
  *   k_cache      [num_blocks][Hkv][D/x][16][x]        x = 16 bytes / element
@@ -102,6 +108,8 @@ typedef struct verify_attn_params {
  *   seq_lens     [num_seqs] int32 S_i, with n_i <= S_i <= max_seq_len and
  *                S_i <= 16 * max_blocks_per_seq (larger values are clamped)
  *   q_start      [num_seqs + 1] int32
+ *   sinks        [Hq] float sink logits in the units of the scaled scores
+ *                (scale * <q, k>), or NULL for none
  *   out          [total_q][Hq][D]                     (dtype); a row with no
  *                visible key (S_i < n_i) is written as zeros
  *   max_q_len    host upper bound on n_i; max_seq_len host upper bound on S_i
@@ -117,8 +125,27 @@ int verify_attention_workspace_size(const verify_attn_params *params, int32_t to
 int verify_attention(const verify_attn_params *params, int32_t total_q, int32_t max_q_len,
                      int32_t max_seq_len, const void *q, const void *k_cache,
                      const void *v_cache, const int32_t *block_tables,
-                     const int32_t *seq_lens, const int32_t *q_start, void *out,
-                     void *workspace, size_t workspace_bytes, hipStream_t stream);
+                     const int32_t *seq_lens, const int32_t *q_start, const float *sinks,
+                     void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * verify_kv_append -- the verify step's new tokens' K and V into the paged
+ * cache (the K/V that verify_attention reads for positions S_i - n_i .. S_i - 1).
+ *
+ * Row j of request i (the token at position p = S_i - n_i + j) is written to
+ * slot p % 16 of block block_tables[i][p / 16], for every KV head, in the
+ * layouts of verify_attention.  params supplies num_seqs, num_kv_heads,
+ * head_dim, block_size, max_blocks_per_seq, num_blocks and dtype (the other
+ * fields are validated as for verify_attention and otherwise unused).
+ *
+ *   k_new, v_new [total_q][Hkv][D] (dtype): the new tokens' keys and values
+ *   k_cache, v_cache: written in place; rows with a negative position or a
+ *                block id outside [0, num_blocks) are skipped
+ * No workspace.  Element bits are copied unchanged.
+ */
+int verify_kv_append(const verify_attn_params *params, int32_t total_q, const void *k_new,
+                     const void *v_new, const int32_t *block_tables, const int32_t *seq_lens,
+                     const int32_t *q_start, void *k_cache, void *v_cache, hipStream_t stream);
 
 /*
  * verify_accept -- vocabulary argmax of each scored position and greedy

@@ -62,7 +62,10 @@ def library(path: Optional[str] = None):
     P = ctypes.POINTER(AttnParams)
     lib.verify_attention_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.verify_attention_workspace_size.restype = ctypes.c_int
-    lib.verify_attention.argtypes = [P, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.verify_attention.argtypes = [P, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.verify_attention.restype = ctypes.c_int
+    lib.verify_kv_append.argtypes = [P, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.verify_kv_append.restype = ctypes.c_int
     lib.verify_attention.restype = ctypes.c_int
     lib.verify_accept_workspace_size.argtypes = [i32, i32, i64, i32, ctypes.POINTER(sz)]
     lib.verify_accept_workspace_size.restype = ctypes.c_int
@@ -154,13 +157,15 @@ def attention_workspace_size(q, k_cache, block_tables, *, max_q_len: int, max_se
 
 def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, max_q_len: int,
                      max_seq_len: int, sliding_window: int = 0, scale: float = 0.0,
-                     kv_split_blocks: int = 0, out=None, workspace=None, stream=None):
+                     kv_split_blocks: int = 0, sinks=None, out=None, workspace=None,
+                     stream=None):
     """Attention of every packed query row against its request's paged KV cache.
 
     q [T, Hq, D]; k_cache [NB, Hkv, D/x, 16, x]; v_cache [NB, Hkv, D, 16] (bf16 or
     fp32, x = 16 bytes / element); block_tables [B, MB], seq_lens [B], q_start
     [B+1] int32 on the device.  max_q_len / max_seq_len are host upper bounds of
-    n_i = q_start[i+1]-q_start[i] and S_i = seq_lens[i].  Returns `out`.
+    n_i = q_start[i+1]-q_start[i] and S_i = seq_lens[i].  sinks: optional [Hq]
+    float32 device tensor of per-head sink logits.  Returns `out`.
     """
     import torch
     params = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
@@ -177,8 +182,9 @@ def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, ma
         ctypes.byref(params), q.shape[0], int(max_q_len), int(max_seq_len),
         _dev_ptr(q, "q"), _dev_ptr(k_cache, "k_cache", q.dtype), _dev_ptr(v_cache, "v_cache", q.dtype),
         _dev_ptr(block_tables, "block_tables", i32), _dev_ptr(seq_lens, "seq_lens", i32),
-        _dev_ptr(q_start, "q_start", i32), _dev_ptr(out, "out", q.dtype),
-        _dev_ptr(workspace, "workspace"), ws_have, _stream_ptr(stream, q.device))
+        _dev_ptr(q_start, "q_start", i32), _dev_ptr(sinks, "sinks", torch.float32),
+        _dev_ptr(out, "out", q.dtype), _dev_ptr(workspace, "workspace"), ws_have,
+        _stream_ptr(stream, q.device))
     _check(rc, "verify_attention")
     return out
 
@@ -261,3 +267,20 @@ def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float
         _dev_ptr(o.get("seq_lens"), "seq_lens", i32), _stream_ptr(stream, dev))
     _check(rc, "verify_budget")
     return o
+
+
+def verify_kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, q_start, *,
+                     stream=None):
+    """Write the new tokens' K/V ([T, Hkv, D], the cache's dtype) into their
+    paged-cache slots (position S_i - n_i + j for row j of request i), in place."""
+    import torch
+    params = _attn_params(torch.empty((0, k_new.shape[1], k_new.shape[2]), dtype=k_new.dtype),
+                          k_cache, block_tables, 0, 0.0, 0)
+    i32 = torch.int32
+    rc = library().verify_kv_append(
+        ctypes.byref(params), k_new.shape[0], _dev_ptr(k_new, "k_new"),
+        _dev_ptr(v_new, "v_new", k_new.dtype), _dev_ptr(block_tables, "block_tables", i32),
+        _dev_ptr(seq_lens, "seq_lens", i32), _dev_ptr(q_start, "q_start", i32),
+        _dev_ptr(k_cache, "k_cache", k_new.dtype), _dev_ptr(v_cache, "v_cache", k_new.dtype),
+        _stream_ptr(stream, k_new.device))
+    _check(rc, "verify_kv_append")

@@ -42,10 +42,19 @@ struct AttnArgs {
     void* out;
     float* part_o;    // [total_q][Hq][max_splits][D]   normalised partial outputs
     float* part_lse;  // [total_q][Hq][max_splits]      log2-sum-exp of each split
+    const float* sinks;  // [Hq] sink logits (natural-log units) or null
     int num_seqs, hq, hkv, group, max_blocks, num_blocks, window, max_seq_len;
     float scale_log2;  // softmax scale * log2(e): scores live in the log2 domain
     int split_blocks, max_splits, row_groups;
 };
+
+// A head's attention sink is one more logit in each row's softmax with a zero
+// value: it adds 2^(sink log2(e) - m) to the row's denominator, with m the
+// maximum the row's sums are relative to (0 without sinks; for a row with no
+// key, m = -inf makes it infinite and the output 0).
+__device__ __forceinline__ float sink_term(const float* sinks, int h, float m) {
+    return sinks ? exp2f(sinks[h] * kLog2e - m) : 0.f;
+}
 
 // Per-request geometry, recomputed identically by every kernel.
 struct SeqGeom {
@@ -220,10 +229,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
         const int rr = r0 + r;
         const int j = rr / a.group, gh = rr - j * a.group;
         const int64_t hrow = (int64_t)(sg.q0 + j) * a.hq + kvh * a.group + gh;
-        const float val = L > 0.f ? O / L : 0.f;
         if (sg.nsplit == 1) {
-            Storage<T>::store(outp, hrow * D + d, val);
+            const float den = L + sink_term(a.sinks, kvh * a.group + gh, M);
+            Storage<T>::store(outp, hrow * D + d, den > 0.f ? O / den : 0.f);
         } else {
+            const float val = L > 0.f ? O / L : 0.f;
             const int64_t pi = hrow * a.max_splits + s;
             a.part_o[pi * D + d] = val;
             if (d == 0) a.part_lse[pi] = L > 0.f ? M + log2f(L) : -INFINITY;
@@ -332,6 +342,7 @@ struct PArgs {
     int nwg;              // workgroups of the persistent launch
     int spb;              // > 0: fixed number of units per workgroup
     int inline_sched;     // 1: attn_persist computes the unit offsets itself
+    const float* sinks;   // [Hq] sink logits (natural-log units) or null
 };
 
 struct MPtrs {
@@ -656,6 +667,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     // that hold the row), thr the raw score above which a lane needs a new
     // maximum, neg_m = -m_r (0 while the row has seen no key).
     float m_r[TPW], l_r[TPW], thr[TPW], neg_m[TPW];
+    float sink_l2[TPW];  // the row's head's sink logit in the log2 domain (-inf: none)
 
     // Pair of cursor c, reached at unit u.
     auto init_pair = [&](const Cursor& c, int u) {
@@ -684,6 +696,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
             l_r[t] = 0.f;
             thr[t] = -INFINITY;
             neg_m[t] = 0.f;
+            sink_l2[t] = a.sinks && valid ? a.sinks[st_g * a.group + gh] * kLog2e : -INFINITY;
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
@@ -707,8 +720,9 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
             const int lr = (wv * TPW + t) * 16 + l16;
             const int rr = st_rg * ROWS + lr;
             if (rr >= rows) continue;
-            const float inv = L > 0.f ? 1.f / L : 0.f;
             if (whole) {
+                const float den = L + (a.sinks ? exp2f(sink_l2[t] - m_r[t]) : 0.f);
+                const float inv = den > 0.f ? 1.f / den : 0.f;
                 const int j = rr / a.group, gh = rr - j * a.group;
                 const int64_t hrow = (int64_t)(srq.q0 + j) * a.hq + st_g * a.group + gh;
 #pragma unroll
@@ -719,6 +733,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
                     *reinterpret_cast<uint2*>(out + hrow * D + d0) = v;
                 }
             } else {
+                const float inv = L > 0.f ? 1.f / L : 0.f;
                 const int64_t srow = slot * ROWS + lr;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt)
@@ -875,6 +890,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
                     acc += f * o[k];
                 }
             }
+            L += sink_term(a.sinks, g * a.group + rr % a.group, M);
             acc *= 1.f / L;
         }
     }
@@ -912,6 +928,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_combine(AttnArgs a, int tot
     if (sg.nsplit > 1) {
         const int64_t pi0 = item * a.max_splits;
         float M = -INFINITY;
+        const int h = (int)(item - (int64_t)row * a.hq);
         for (int s = 0; s < sg.nsplit; ++s) M = fmaxf(M, a.part_lse[pi0 + s]);
         if (M != -INFINITY) {
             for (int s = 0; s < sg.nsplit; ++s) {
@@ -923,11 +940,45 @@ __global__ __launch_bounds__(kAttnThreads) void attn_combine(AttnArgs a, int tot
 #pragma unroll
                 for (int e = 0; e < DPL; ++e) acc[e] = fmaf(f, po[e], acc[e]);
             }
+            L += sink_term(a.sinks, h, M);
         }
     }
 #pragma unroll
     for (int e = 0; e < DPL; ++e)
         Storage<T>::store(outp, item * D + lane * DPL + e, L > 0.f ? acc[e] / L : 0.f);
+}
+
+// ------------------------------------------------------------------ KV append
+//
+// The verify step's new tokens (row j of request i sits at position
+// p = S_i - n_i + j) get their K and V written into slot p % 16 of block
+// block_tables[i][p / 16]: K x-packed ([D/x][16][x] per block and head), V
+// transposed ([D][16]).  One workgroup per (row, KV head); thread d moves
+// dimension d.  Rows with a negative position or a block id outside
+// [0, num_blocks) are skipped.
+template <typename T, int D>
+__global__ __launch_bounds__(D) void attn_kv_append(
+    int num_seqs, int hkv, int max_blocks, int num_blocks, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, const int32_t* __restrict__ block_tables,
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start, T* __restrict__ kc,
+    T* __restrict__ vc) {
+    constexpr int X = Storage<T>::kPer16B;
+    const int row = blockIdx.x, g = blockIdx.y, d = threadIdx.x;
+    int lo = 0, hi = num_seqs - 1;  // request owning the row: largest i with q_start[i] <= row
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (q_start[mid] <= row) lo = mid; else hi = mid - 1;
+    }
+    const int n = q_start[lo + 1] - q_start[lo];
+    const int64_t p = (int64_t)seq_lens[lo] - n + (row - q_start[lo]);
+    if (p < 0 || p / kBlockTokens >= max_blocks) return;
+    const int b = block_tables[(int64_t)lo * max_blocks + p / kBlockTokens];
+    if (b < 0 || b >= num_blocks) return;
+    const int t = (int)(p % kBlockTokens);
+    const int64_t src = ((int64_t)row * hkv + g) * D + d;
+    const int64_t bh = (int64_t)b * hkv + g;
+    kc[((bh * (D / X) + d / X) * kBlockTokens + t) * X + d % X] = k_new[src];
+    vc[(bh * D + d) * kBlockTokens + t] = v_new[src];
 }
 
 // ------------------------------------------------------------------ host side
@@ -1170,8 +1221,8 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
                                 int32_t max_q_len, int32_t max_seq_len, const void* q,
                                 const void* k_cache, const void* v_cache,
                                 const int32_t* block_tables, const int32_t* seq_lens,
-                                const int32_t* q_start, void* out, void* workspace,
-                                size_t workspace_bytes, hipStream_t stream) {
+                                const int32_t* q_start, const float* sinks, void* out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
     int rc = validate(params, total_q, max_q_len, max_seq_len);
     if (rc != VERIFY_OK) return rc;
     const verify_attn_params& p = *params;
@@ -1216,6 +1267,7 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         a.nwg = pl.nwg;
         a.spb = pl.spb;
         a.inline_sched = p.num_seqs <= kInlineSchedSeqs;
+        a.sinks = sinks;
         if (!launch_persist(a, m, pl, p.head_dim, stream)) return VERIFY_EUNSUPPORTED;
         return check_launch();
     }
@@ -1244,8 +1296,36 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
     a.split_blocks = pl.split_blocks;
     a.max_splits = pl.max_splits;
     a.row_groups = pl.row_groups;
+    a.sinks = sinks;
     if (p.head_dim == 128) launch_valu<float, 128>(a, pl, total_q, stream);
     else launch_valu<float, 64>(a, pl, total_q, stream);
+    return check_launch();
+}
+
+extern "C" int verify_kv_append(const verify_attn_params* params, int32_t total_q,
+                                const void* k_new, const void* v_new, const int32_t* block_tables,
+                                const int32_t* seq_lens, const int32_t* q_start, void* k_cache,
+                                void* v_cache, hipStream_t stream) {
+    int rc = validate(params, total_q, 0, 0);
+    if (rc != VERIFY_OK) return rc;
+    const verify_attn_params& p = *params;
+    if (total_q == 0 || p.num_seqs == 0) return VERIFY_OK;
+    if (!k_new || !v_new || !block_tables || !seq_lens || !q_start || !k_cache || !v_cache)
+        return VERIFY_EINVAL;
+    const dim3 grid((unsigned)total_q, (unsigned)p.num_kv_heads);
+#define AVERIFY_APPEND(T, D)                                                                       \
+    hipLaunchKernelGGL((attn_kv_append<T, D>), grid, dim3(D), 0, stream, p.num_seqs, p.num_kv_heads, \
+                       p.max_blocks_per_seq, p.num_blocks, static_cast<const T*>(k_new),          \
+                       static_cast<const T*>(v_new), block_tables, seq_lens, q_start,             \
+                       static_cast<T*>(k_cache), static_cast<T*>(v_cache))
+    if (p.dtype == VERIFY_BF16) {
+        if (p.head_dim == 128) AVERIFY_APPEND(uint16_t, 128);
+        else AVERIFY_APPEND(uint16_t, 64);
+    } else {
+        if (p.head_dim == 128) AVERIFY_APPEND(float, 128);
+        else AVERIFY_APPEND(float, 64);
+    }
+#undef AVERIFY_APPEND
     return check_launch();
 }
 
@@ -1260,4 +1340,4 @@ extern "C" const char* verify_status_string(int status) {
     }
 }
 
-extern "C" int verify_abi_version(void) { return 10000; }
+extern "C" int verify_abi_version(void) { return 10100; }

@@ -37,9 +37,9 @@ def to_host_f64(t) -> np.ndarray:
     return t.detach().to(torch.float64).cpu().numpy()
 
 
-def gpu_attention(q, kc, vc, bt, sl, qs, *, max_q_len, max_seq_len, window=0, split=0):
+def gpu_attention(q, kc, vc, bt, sl, qs, *, max_q_len, max_seq_len, window=0, split=0, sinks=None):
     out = av.verify_attention(q, kc, vc, bt, sl, qs, max_q_len=max_q_len, max_seq_len=max_seq_len,
-                              sliding_window=window, kv_split_blocks=split)
+                              sliding_window=window, kv_split_blocks=split, sinks=sinks)
     torch.cuda.synchronize()
     return out
 
@@ -69,7 +69,8 @@ def compact_for_rows(batch, layer, rows: np.ndarray):
     args = dict(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads, head_dim=cfg.head_dim,
                 sliding_window=layer.window, scale=0.0, dtype=workload.dtype_code(cfg.dtype),
                 q=q_c, k_cache=kc, v_cache=vc, block_tables=bt_c,
-                seq_lens=batch.seq_lens[reqs], q_start=qs_c)
+                seq_lens=batch.seq_lens[reqs], q_start=qs_c,
+                sinks=None if layer.sinks is None else layer.sinks.cpu().numpy())
     return args, rows_c
 
 

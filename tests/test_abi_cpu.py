@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10000
+    assert av.abi_version() == 10100
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
@@ -80,7 +80,7 @@ def test_attention_argument_validation(kw, want):
     rc, _ = _ws(_params(**kw))
     assert rc == want
     # the launch entry point reports the same status (it validates first)
-    rc2 = av.library().verify_attention(ctypes.byref(_params(**kw)), 36, 9, 1000, *([None] * 7),
+    rc2 = av.library().verify_attention(ctypes.byref(_params(**kw)), 36, 9, 1000, *([None] * 8),
                                         None, 0, None)
     assert rc2 == want
 
@@ -106,11 +106,11 @@ def test_attention_workspace_query_and_checks():
     dummy = ctypes.c_void_p(0x1000)
     for kw, need in ((dict(dtype=av.F32, kv_split_blocks=8), n), (dict(kv_split_blocks=8), b)):
         rc = lib.verify_attention(ctypes.byref(_params(**kw)), 36, 9, 1000, dummy, dummy, dummy,
-                                  dummy, dummy, dummy, dummy, dummy, need - 1, None)
+                                  dummy, dummy, dummy, None, dummy, dummy, need - 1, None)
         assert rc == av.EWORKSPACE
     # null required pointers
     rc = lib.verify_attention(ctypes.byref(_params()), 36, 9, 1000, None, dummy, dummy, dummy,
-                              dummy, dummy, dummy, dummy, auto, None)
+                              dummy, dummy, None, dummy, dummy, auto, None)
     assert rc == av.EINVAL
     # negative host sizes
     assert _ws(_params(), total_q=-1)[0] == av.EINVAL
@@ -170,3 +170,18 @@ def test_budget_argument_validation():
     assert call(cx=d) == av.EINVAL                    # ctx_len without seq_lens
     assert call(sl=d) == av.EINVAL                    # seq_lens without ctx_len
     assert call(num_seqs=1 << 20, max_len=4096, cap=1 << 40) == av.EUNSUPPORTED
+
+
+def test_kv_append_argument_validation():
+    lib = av.library()
+    d = ctypes.c_void_p(0x1000)
+    for kw, want in ((dict(head_dim=96), av.EUNSUPPORTED), (dict(num_kv_heads=0), av.EINVAL),
+                     (dict(dtype=7), av.EUNSUPPORTED)):
+        assert lib.verify_kv_append(ctypes.byref(_params(**kw)), 36, d, d, d, d, d, d, d, None) == want
+    for i in range(7):
+        ptrs = [d] * 7
+        ptrs[i] = None
+        assert lib.verify_kv_append(ctypes.byref(_params()), 36, *ptrs, None) == av.EINVAL
+    assert lib.verify_kv_append(ctypes.byref(_params()), -1, d, d, d, d, d, d, d, None) == av.EINVAL
+    # nothing to append: a no-op that needs no pointers
+    assert lib.verify_kv_append(ctypes.byref(_params()), 0, *([None] * 7), None) == 0

@@ -227,7 +227,7 @@ def test_attention_full_size_sampled(name):
     for layer in bt.layers:
         out = gpu_attention(layer.q, layer.k_cache, layer.v_cache, bt.t_block_tables,
                             bt.t_seq_lens, bt.t_q_start, max_q_len=bt.max_q_len,
-                            max_seq_len=bt.max_seq_len, window=layer.window)
+                            max_seq_len=bt.max_seq_len, window=layer.window, sinks=layer.sinks)
         got = to_host_f64(out[torch.as_tensor(rows, device=DEV, dtype=torch.int64),
                               torch.as_tensor(heads, device=DEV, dtype=torch.int64)])
         args, rows_c = compact_for_rows(bt, layer, rows)

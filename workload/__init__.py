@@ -15,7 +15,8 @@ Inputs follow the recipe of the workloads the paper measures (Sec. 5.1: agentic
 code generation, deep research, SWE-Bench and GAIA traces, which are not
 available here); shapes follow the models the paper serves (Qwen-3-8B,
 DeepSeek-R1-Distill-Llama-8B, GPT-OSS-20B):
-  * Q, K, V ~ N(0, 1), drawn in fp32 and rounded to the storage dtype;
+  * Q, K, V ~ N(0, 1), drawn in fp32 and rounded to the storage dtype; the
+    GPT-OSS-shaped workload adds per-head attention sink logits ~ N(0, 1);
   * the paged KV cache holds sum_i ceil(S_i/16) physical 16-token blocks, handed
     to requests through a random permutation (fragmented placement);
   * logits ~ N(0, 1) i.i.d. per row, with the position of the row maximum drawn
@@ -54,6 +55,7 @@ class Config:
     drafts: Tuple                   # ("fixed", k) | ("choice", (k, ...)) | ("uniform", lo, hi)
     match: Tuple                    # ("divergence",) | ("prob", p) | ("halves", p_first, p_second)
     windows: Tuple[int, ...] = (0,)  # one attention layer per entry; 0 = full causal
+    sinks: bool = False             # per-head attention sink logits in every layer
     description: str = ""
 
     def replace(self, **kw) -> "Config":
@@ -82,8 +84,9 @@ CONFIGS = {
     "gpt_oss_20b": Config(
         name="gpt_oss_20b", batch=64, num_q_heads=64, num_kv_heads=8, head_dim=64, dtype="bf16",
         vocab=201088, context=("uniform", 4096, 65536), drafts=("fixed", 8), match=("prob", 0.5),
-        windows=(128, 0),
-        description="GPT-OSS-20B-shaped verify step: a 128-token sliding-window layer and a full layer"),
+        windows=(128, 0), sinks=True,
+        description="GPT-OSS-20B-shaped verify step: a 128-token sliding-window layer and a full "
+                    "layer, both with per-head attention sinks"),
     "long_context": Config(
         name="long_context", batch=128, num_q_heads=32, num_kv_heads=8, head_dim=128,
         dtype="bf16", vocab=151936, context=("uniform", 32768, 131072), drafts=("uniform", 0, 32),
@@ -98,6 +101,7 @@ class Layer:
     q: object          # torch tensor [T, Hq, D]
     k_cache: object    # torch tensor [num_blocks, Hkv, D/x, 16, x]
     v_cache: object    # torch tensor [num_blocks, Hkv, D, 16]
+    sinks: object = None  # torch float32 [Hq] sink logits, or None
 
 
 @dataclass
@@ -315,7 +319,11 @@ def make_batch(cfg: Config, seed: int, device: str = "cpu", *,
             q = torch.randn((T, Hq, D), generator=g, device=device, dtype=torch.float32).to(dt)
             kc = _randn_storage((num_blocks, Hkv, D // x, BLOCK, x), g, device, dt)
             vc = _randn_storage((num_blocks, Hkv, D, BLOCK), g, device, dt)
-            batch.layers.append(Layer(window=w, q=q, k_cache=kc, v_cache=vc))
+            # sink logits ~ N(0, 1), drawn after the caches so that adding them
+            # leaves every other tensor of the stream unchanged
+            sk = (torch.randn(Hq, generator=g, device=device, dtype=torch.float32)
+                  if cfg.sinks else None)
+            batch.layers.append(Layer(window=w, q=q, k_cache=kc, v_cache=vc, sinks=sk))
     return batch
 
 
