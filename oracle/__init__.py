@@ -13,6 +13,8 @@ Functions (each restates the paper's definition; see ``oracle.c``):
                      k+1 positions in one target pass, Sec. 2.2).
   kv_append(...)  -- the new tokens' K/V written into their paged-cache slots.
   argmax(...)     -- lowest index of the row maximum, plus the top-2 gap.
+  sample(...)     -- stochastic verification's per-row sample from softmax(x/T)
+                     (Gumbel-max with Philox4x32-10 noise).
   accept(...)     -- greedy acceptance: longest matching draft prefix plus one
                      bonus token; rejection rate = rejected / proposed (Sec. 3.1).
   budget(...)     -- redundancy-aware draft budget (Sec. 4.2, Alg. 2) and the
@@ -68,6 +70,13 @@ def _load():
     lib.oracle_budget.argtypes = [i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp, vp,
                                   vp]
     lib.oracle_budget.restype = ctypes.c_int
+    lib.oracle_sample.argtypes = [i64, i64, i64, i32, vp, ctypes.c_float, ctypes.c_uint64,
+                                  ctypes.c_uint32, vp]
+    lib.oracle_sample.restype = ctypes.c_int
+    lib.oracle_philox4x32_10.argtypes = [vp, vp, vp]
+    lib.oracle_philox4x32_10.restype = None
+    lib.oracle_sample_log.argtypes = [i64, vp, vp]
+    lib.oracle_sample_log.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -167,6 +176,42 @@ def argmax(logits, dtype: int, with_gap: bool = True):
     if rc != 0:
         raise ValueError("oracle_argmax rejected its arguments")
     return am, gap
+
+
+def inv_temperature(temperature: float) -> np.float32:
+    """The fp32 1/T both sides multiply the logits by."""
+    return np.float32(1.0 / float(temperature))
+
+
+def sample(logits, dtype: int, temperature: float, seed: int, offset: int = 0) -> np.ndarray:
+    """Each row's token drawn from softmax(logits / T) by the Gumbel-max rule
+    (see oracle_sample): the stochastic verification's per-row sample."""
+    lib = _load()
+    lg = _raw(logits, dtype)
+    rows, vocab = lg.shape
+    out = np.zeros(rows, dtype=np.int32)
+    rc = lib.oracle_sample(rows, vocab, vocab, dtype, _ptr(lg), float(inv_temperature(temperature)),
+                           int(seed) & ((1 << 64) - 1), int(offset) & 0xFFFFFFFF, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_sample rejected its arguments")
+    return out
+
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    """One Philox4x32-10 block: 4 counter words, 2 key words -> 4 output words."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    _load().oracle_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def sample_log(x) -> np.ndarray:
+    """The fp32 natural log the sampler's Gumbel noise uses."""
+    a = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.zeros_like(a)
+    _load().oracle_sample_log(a.size, _ptr(a), _ptr(out))
+    return out
 
 
 def accept(q_start, tokens, argmax_rows):

@@ -19,6 +19,9 @@
  *   oracle_kv_append  -- the new tokens' K/V written into their cache slots.
  *   oracle_argmax     -- per logits row, the lowest index attaining the maximum
  *                        (plus the gap to the runner-up, for near-tie flags).
+ *   oracle_sample     -- each row's token drawn from softmax(logits / T) by the
+ *                        Gumbel-max rule (Philox4x32-10 noise), the stochastic
+ *                        verification's replacement for the argmax.
  *   oracle_accept     -- greedy acceptance: the longest prefix of drafts equal
  *                        to the target's argmax, followed by one bonus token.
  *   oracle_budget     -- redundancy-aware draft budget (Sec. 4.2, Alg. 2): the
@@ -185,6 +188,109 @@ int oracle_argmax(int64_t rows, int64_t vocab, int64_t row_stride, int32_t dtype
             }
             gap[r] = vocab == 1 ? INFINITY : bestv - second;
         }
+    }
+    return 0;
+}
+
+/*
+ * Stochastic verification (temperature T > 0).  With drafts that put all of
+ * their probability on one token (the suffix / n-gram style drafts of Sec. 2.2
+ * and 4.1), speculative rejection sampling accepts draft d with probability
+ * p(d) and, on a rejection, draws from p with d's mass removed; sampling
+ * y ~ p = softmax(logits / T) and accepting iff y == d (emitting y otherwise)
+ * does exactly that.  So the stochastic step is the greedy one with each row's
+ * argmax replaced by a sample, drawn by the Gumbel-max rule
+ *     y = argmax_v ( x_v / T + g_v ),   g_v = -log(-log(u_v)),  u_v ~ U(0, 1),
+ * ties to the lowest index, a NaN logit maximal (as in oracle_argmax).
+ *
+ * u_v comes from Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011): key
+ * (seed low word, seed high word), counter (v / 4, row, offset, 0), output word
+ * v % 4, mapped to ((w >> 8) + 0.5) * 2^-24.  The score is computed in fp32
+ * as fmaf(x, inv_temperature, g) with g from sample_log below, so that an
+ * implementation making the same fp32 operations draws the same tokens.
+ */
+static void philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Natural log in fp32 for x > 0 normal: x = m 2^e with m in [sqrt(1/2), sqrt(2)),
+ * log x = e ln 2 + 2 atanh(z), z = (m - 1) / (m + 1), the atanh series to z^9
+ * (|z| <= 0.1716, truncation below 1e-9). */
+static float sample_log(float x)
+{
+    uint32_t bits;
+    memcpy(&bits, &x, 4);
+    int e = (int)((bits >> 23) & 0xFF) - 127;
+    uint32_t mb = (bits & 0x7FFFFFu) | 0x3F800000u;
+    float m;
+    memcpy(&m, &mb, 4);
+    if (m > 1.41421354f) { m = m * 0.5f; e += 1; }
+    const float z = (m - 1.0f) / (m + 1.0f);
+    const float z2 = z * z;
+    float poly = fmaf(z2, 0.111111112f, 0.142857149f);
+    poly = fmaf(z2, poly, 0.200000003f);
+    poly = fmaf(z2, poly, 0.333333343f);
+    poly = fmaf(z2, poly, 1.0f);
+    const float r = 2.0f * z * poly;
+    return fmaf((float)e, 0.693147182f, r);
+}
+
+static float sample_uniform(uint32_t w) { return ((float)(w >> 8) + 0.5f) * 5.96046448e-08f; }
+
+static float gumbel_noise(uint64_t seed, uint32_t offset, int64_t row, int64_t v)
+{
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    const uint32_t ctr[4] = {(uint32_t)(v >> 2), (uint32_t)row, offset, 0u};
+    uint32_t out[4];
+    philox4x32_10(ctr, key, out);
+    const float u = sample_uniform(out[v & 3]);
+    return -sample_log(-sample_log(u));
+}
+
+/* Test hooks for the generator and the log: the raw Philox block, and
+ * sample_log applied elementwise. */
+void oracle_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out)
+{
+    philox4x32_10(ctr, key, out);
+}
+
+void oracle_sample_log(int64_t n, const float *x, float *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = sample_log(x[i]);
+}
+
+int oracle_sample(int64_t rows, int64_t vocab, int64_t row_stride, int32_t dtype,
+                  const void *logits, float inv_temperature, uint64_t seed, uint32_t offset,
+                  int32_t *sampled)
+{
+    if (vocab <= 0 || vocab > 0x7fffffff || !(inv_temperature > 0.0f)) return -1;
+    if (row_stride == 0) row_stride = vocab;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        const int64_t base = r * row_stride;
+        int64_t best = 0;
+        float bestv = 0.0f;
+        for (int64_t v = 0; v < vocab; ++v) {
+            const float x = (float)elem_to_double(logits, dtype, base + v);
+            if (isnan(x)) { best = v; break; }
+            const float sc = fmaf(x, inv_temperature, gumbel_noise(seed, offset, r, v));
+            if (v == 0 || sc > bestv) { best = v; bestv = sc; }
+        }
+        sampled[r] = (int32_t)best;
     }
     return 0;
 }
