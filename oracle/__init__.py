@@ -77,6 +77,8 @@ def _load():
     lib.oracle_philox4x32_10.restype = None
     lib.oracle_sample_log.argtypes = [i64, vp, vp]
     lib.oracle_sample_log.restype = None
+    lib.oracle_gumbel_of_word.argtypes = [i64, vp, vp, vp]
+    lib.oracle_gumbel_of_word.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -212,6 +214,16 @@ def sample_log(x) -> np.ndarray:
     out = np.zeros_like(a)
     _load().oracle_sample_log(a.size, _ptr(a), _ptr(out))
     return out
+
+
+def gumbel_of_word(w):
+    """(u, g): the uniform and the Gumbel noise term the sampler derives from
+    raw Philox output words."""
+    a = np.ascontiguousarray(w, dtype=np.uint32)
+    u = np.zeros(a.shape, dtype=np.float32)
+    g = np.zeros(a.shape, dtype=np.float32)
+    _load().oracle_gumbel_of_word(a.size, _ptr(a), _ptr(u), _ptr(g))
+    return u, g
 
 
 def accept(q_start, tokens, argmax_rows):

@@ -37,7 +37,8 @@
  *     aligned causal mask inside the draft);
  *   - a sliding window W > 0 keeps keys with p - W < t <= p;
  *   - query head h reads KV head floor(h / (Hq / Hkv)) (grouped-query);
- *   - scale defaults to 1/sqrt(head_dim); no soft-cap, no bias, no sinks;
+ *   - scale defaults to 1/sqrt(head_dim); no soft-cap, no bias; attention
+ *     sinks only when given (see oracle_attention);
  *   - a row with no visible key (only possible when S < n) yields zeros.
  *
  * Paged KV layout read here (element index, x = 16 bytes / element size):
@@ -205,7 +206,11 @@ int oracle_argmax(int64_t rows, int64_t vocab, int64_t row_stride, int32_t dtype
  *
  * u_v comes from Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011): key
  * (seed low word, seed high word), counter (v / 4, row, offset, 0), output word
- * v % 4, mapped to ((w >> 8) + 0.5) * 2^-24.  The score is computed in fp32
+ * v % 4, mapped to u = ((w >> 9) + 0.5) * 2^-23 = (2 (w >> 9) + 1) * 2^-24: the top
+ * 23 bits, so that u is an odd multiple of 2^-24 that fp32 holds exactly, in
+ * [2^-24, 1 - 2^-24].  (With 24 bits the sum (w >> 8) + 0.5 needs 25
+ * significant bits and rounds, and the top code would give u = 1 and an
+ * unbounded noise term.)  The score is computed in fp32
  * as fmaf(x, inv_temperature, g) with g from sample_log below, so that an
  * implementation making the same fp32 operations draws the same tokens.
  */
@@ -249,7 +254,7 @@ static float sample_log(float x)
     return fmaf((float)e, 0.693147182f, r);
 }
 
-static float sample_uniform(uint32_t w) { return ((float)(w >> 8) + 0.5f) * 5.96046448e-08f; }
+static float sample_uniform(uint32_t w) { return ((float)(w >> 9) + 0.5f) * 0x1p-23f; }
 
 static float gumbel_noise(uint64_t seed, uint32_t offset, int64_t row, int64_t v)
 {
@@ -261,8 +266,8 @@ static float gumbel_noise(uint64_t seed, uint32_t offset, int64_t row, int64_t v
     return -sample_log(-sample_log(u));
 }
 
-/* Test hooks for the generator and the log: the raw Philox block, and
- * sample_log applied elementwise. */
+/* Test hooks for the generator and the log: the raw Philox block, sample_log
+ * applied elementwise, and the noise term g of a raw Philox output word. */
 void oracle_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out)
 {
     philox4x32_10(ctr, key, out);
@@ -271,6 +276,14 @@ void oracle_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *ou
 void oracle_sample_log(int64_t n, const float *x, float *out)
 {
     for (int64_t i = 0; i < n; ++i) out[i] = sample_log(x[i]);
+}
+
+void oracle_gumbel_of_word(int64_t n, const uint32_t *w, float *u, float *g)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        u[i] = sample_uniform(w[i]);
+        g[i] = -sample_log(-sample_log(u[i]));
+    }
 }
 
 int oracle_sample(int64_t rows, int64_t vocab, int64_t row_stride, int32_t dtype,

@@ -123,3 +123,32 @@ def test_special_rows():
     x[2, 3] = 0.0
     s = oracle.sample(x, oracle.F32, 0.7, seed=1)
     assert s.tolist() == [5, 0, 3]
+
+
+def test_noise_term_is_bounded_and_monotone():
+    # the uniform is an odd multiple of 2^-24 strictly inside (0, 1) for every
+    # word, so the noise is finite, increasing in the word, and at its extremes
+    # -log(-log(u)) of the extreme uniforms
+    top = np.arange(0, 1 << 23, 997, dtype=np.uint64)
+    w = np.concatenate([(top << 9), (top << 9) | 0x1FF,
+                        [0, 1, 0x1FF, 0xFFFFFE00, 0xFFFFFFFF, 0x80000000, 0x7FFFFFFF]]).astype(np.uint32)
+    u, g = oracle.gumbel_of_word(w)
+    k = (w >> 9).astype(np.float64)
+    np.testing.assert_array_equal(u.astype(np.float64), (2 * k + 1) * 2.0 ** -24)
+    assert np.all((u > 0) & (u < 1)) and np.all(np.isfinite(g))
+    order = np.argsort(w, kind="stable")
+    assert np.all(np.diff(g[order].astype(np.float64)) >= 0)
+    lo, hi = oracle.gumbel_of_word(np.uint32([0, 0xFFFFFFFF]))[1].astype(np.float64)
+    assert abs(lo - (-math.log(-math.log(2.0 ** -24)))) < 1e-5
+    assert abs(hi - (-math.log(-math.log1p(-2.0 ** -24)))) < 1e-4 * 16.6
+
+
+def test_dominant_logit_wins_every_row_of_a_large_vocabulary():
+    # one token 30 nats above 131071 others: every other token together has
+    # probability 131071 e^-30 ~ 1e-8 per row, so 400 rows all draw the
+    # dominant token; an unbounded noise term (u rounding to 1) would not
+    V, R = 1 << 17, 400
+    x = np.zeros((R, V), dtype=np.float32)
+    x[:, 777] = 30.0
+    s = oracle.sample(x, oracle.F32, 1.0, seed=2024, offset=0)
+    assert np.all(s == 777), int((s != 777).sum())
