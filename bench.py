@@ -189,6 +189,34 @@ def kv_append_timing(av, bt, steps: int):
     return {"us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rows": T}
 
 
+def accept_timing(av, bt, steps: int, aws):
+    """Device time of the acceptance calls on the step's logits: greedy
+    (verify_accept) and stochastic at T = 0.7 (verify_accept_sampled), with
+    the logits' bytes per microsecond each reaches.  The sampled call scores
+    every logit with its own Gumbel noise, so it is bound by vector ALU work,
+    not by HBM."""
+    import torch
+    T, V = bt.logits.shape
+    dev = bt.logits.device
+    B = len(bt.q_start) - 1
+    outs = [torch.empty(n, dtype=torch.int32, device=dev) for n in (B, B, T, T)]
+    greedy = lambda: av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start, accept_len=outs[0],
+                                      num_emitted=outs[1], emitted=outs[2], argmax_out=outs[3],
+                                      workspace=aws)
+    sampled = lambda: av.verify_accept_sampled(bt.logits, bt.t_tokens, bt.t_q_start, temperature=0.7,
+                                               seed=1234, offset=1, accept_len=outs[0],
+                                               num_emitted=outs[1], emitted=outs[2],
+                                               sampled_out=outs[3], workspace=aws)
+    nbytes = T * V * bt.logits.element_size()
+    res = {"logits_bytes": nbytes, "rows": T, "vocab": V}
+    for name, fn in (("greedy", greedy), ("sampled_T0.7", sampled)):
+        fn()
+        us = graph_time_us(fn, steps)
+        res[name] = {"us": us, "GBps": nbytes / (us * 1e-6) / 1e9,
+                     "logits_per_ns": T * V / (us * 1e3)}
+    return res
+
+
 def budget_timing(av, workload, *, oracle_ok: bool, batch: int, steps: int, dev: str):
     """Mean device time of one verify_budget call (Sec. 4.2, Alg. 2) on seeded
     candidate sets for the batch, and the oracle's time for the same call.  The
@@ -415,6 +443,8 @@ def main():
     log("budget allocation (verify_budget):", budget)
     append = kv_append_timing(av, bt, K)
     log("KV append (verify_kv_append):", append)
+    accept_t = accept_timing(av, bt, K, aws)
+    log("acceptance calls:", accept_t)
 
     traffic = stored_traffic(cfg.name)
     if traffic is not None:
@@ -456,6 +486,7 @@ def main():
         "cpu_baseline": cpu,
         "budget_alloc": budget,
         "kv_append": append,
+        "accept": accept_t,
     }
     print(json.dumps(res), flush=True)
 

@@ -22,6 +22,10 @@
  *                       step's q_start / tokens / seq_lens built from them.
  *   verify_kv_append -- the n_i new tokens' K/V written into their cache slots
  *                       before verify_attention reads them.
+ *   verify_accept_sampled -- verify_accept at a temperature T > 0: each row
+ *                       draws its token from softmax(logits / T) instead of
+ *                       taking the argmax (speculative sampling with drafts
+ *                       that are single tokens).
  *
  * Conventions shared by both calls
  * --------------------------------
@@ -176,6 +180,44 @@ int verify_accept(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_
                   const int32_t *q_start, int32_t *argmax_out, int32_t *accept_len,
                   int32_t *num_emitted, int32_t *emitted, void *workspace,
                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * verify_accept_sampled -- stochastic verification at temperature T > 0
+ * (Sec. 2.2: the speculative output follows the target's distribution).
+ *
+ * The drafts are single tokens, i.e. proposals with all their probability on
+ * one token.  Speculative rejection sampling then accepts draft d at row r
+ * with probability p_r(d), p_r = softmax(logits[r] / T), and on rejection
+ * emits a token from p_r with d removed.  Drawing y_r ~ p_r and accepting
+ * iff y_r == d is the same rule, so the call draws one y_r per row and runs
+ * verify_accept's acceptance with y in place of the argmax.
+ *
+ * y_r = argmax_v (x_v * inv_T + g_v) (the Gumbel-max rule), where
+ *   inv_T = (float)(1.0 / (double)temperature);
+ *   g_v   = -log(-log u_v), u_v = ((w >> 9) + 0.5) * 2^-23 (exact in fp32);
+ *   w     = word (v mod 4) of Philox4x32-10 (Salmon et al., SC 2011) with key
+ *           (seed mod 2^32, seed >> 32) and counter (v / 4, r, offset, 0);
+ *   log   = an fp32 atanh-series log: x = m 2^e with m in [sqrt(2)/2, sqrt(2)),
+ *           z = (m - 1) / (m + 1), log x = e ln2 + 2 z (1 + z^2 (1/3 + z^2 (1/5
+ *           + z^2 (1/7 + z^2 / 9)))), every step one fp32 operation (the
+ *           products with fused multiply-add as written).
+ * The draw is therefore a pure function of (logits, temperature, seed, offset,
+ * row index) and is reproduced bit for bit by any implementation of those
+ * steps.  NaN logits and ties follow verify_accept: the first NaN wins, equal
+ * scores go to the lower index.  Rows are independent draws as long as
+ * (seed, offset) is not reused; use offset for the decoding step.
+ *
+ *   temperature  finite, > 0 (VERIFY_EINVAL otherwise)
+ *   sampled_out  [total_q] int32 or NULL: the drawn y_r
+ * All other arguments, the workspace size and the outputs are verify_accept's,
+ * with y in place of the argmax.
+ */
+int verify_accept_sampled(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_stride,
+                          int32_t logits_dtype, const void *logits, const int32_t *tokens,
+                          const int32_t *q_start, float temperature, uint64_t seed,
+                          uint32_t offset, int32_t *sampled_out, int32_t *accept_len,
+                          int32_t *num_emitted, int32_t *emitted, void *workspace,
+                          size_t workspace_bytes, hipStream_t stream);
 
 /*
  * verify_budget -- redundancy-aware draft budget (Sec. 4.2, Alg. 2).

@@ -66,11 +66,13 @@ def library(path: Optional[str] = None):
     lib.verify_attention.restype = ctypes.c_int
     lib.verify_kv_append.argtypes = [P, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.verify_kv_append.restype = ctypes.c_int
-    lib.verify_attention.restype = ctypes.c_int
     lib.verify_accept_workspace_size.argtypes = [i32, i32, i64, i32, ctypes.POINTER(sz)]
     lib.verify_accept_workspace_size.restype = ctypes.c_int
     lib.verify_accept.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.verify_accept.restype = ctypes.c_int
+    lib.verify_accept_sampled.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, ctypes.c_float,
+                                          ctypes.c_uint64, ctypes.c_uint32, vp, vp, vp, vp, vp, sz, vp]
+    lib.verify_accept_sampled.restype = ctypes.c_int
     f64 = ctypes.c_double
     lib.verify_budget.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp,
                                   vp, i64, vp, vp]
@@ -197,13 +199,7 @@ def accept_workspace_size(num_seqs: int, total_q: int, vocab: int, dtype_code: i
     return int(n.value)
 
 
-def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, num_emitted=None,
-                  emitted=None, workspace=None, stream=None):
-    """Vocabulary argmax of every row and greedy acceptance of the drafts.
-
-    logits [T, V] (bf16 or fp32), tokens [T] and q_start [B+1] int32 on the
-    device.  Returns (accept_len [B], num_emitted [B], emitted [T], argmax [T]).
-    """
+def _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace):
     import torch
     T, V = logits.shape
     B = q_start.shape[0] - 1
@@ -222,14 +218,55 @@ def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, 
     if workspace is None and ws_bytes > 0:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     ws_have = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return B, T, V, code, argmax_out, accept_len, num_emitted, emitted, workspace, ws_have
+
+
+def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, num_emitted=None,
+                  emitted=None, workspace=None, stream=None):
+    """Vocabulary argmax of every row and greedy acceptance of the drafts.
+
+    logits [T, V] (bf16 or fp32), tokens [T] and q_start [B+1] int32 on the
+    device.  Returns (accept_len [B], num_emitted [B], emitted [T], argmax [T]).
+    """
+    import torch
+    i32 = torch.int32
+    B, T, V, code, argmax_out, accept_len, num_emitted, emitted, workspace, ws_have = \
+        _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace)
     rc = library().verify_accept(
         B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
         _dev_ptr(q_start, "q_start", i32), _dev_ptr(argmax_out, "argmax_out", i32),
         _dev_ptr(accept_len, "accept_len", i32), _dev_ptr(num_emitted, "num_emitted", i32),
         _dev_ptr(emitted, "emitted", i32), _dev_ptr(workspace, "workspace"), ws_have,
-        _stream_ptr(stream, dev))
+        _stream_ptr(stream, logits.device))
     _check(rc, "verify_accept")
     return accept_len, num_emitted, emitted, argmax_out
+
+
+def verify_accept_sampled(logits, tokens, q_start, *, temperature: float, seed: int, offset: int = 0,
+                          sampled_out=None, accept_len=None, num_emitted=None, emitted=None,
+                          workspace=None, stream=None):
+    """Stochastic verification at temperature T > 0: every row draws
+    y ~ softmax(logits / T) (Gumbel-max with Philox4x32-10 noise keyed by
+    `seed`, counter (v / 4, row, offset, 0)) and a request accepts its drafts
+    up to the first one that differs from its row's draw.
+
+    Same layouts as verify_accept.  Returns (accept_len [B], num_emitted [B],
+    emitted [T], sampled [T]).
+    """
+    import torch
+    i32 = torch.int32
+    if not 0 <= int(seed) < (1 << 64) or not 0 <= int(offset) < (1 << 32):
+        raise ValueError("seed must fit 64 bits and offset 32 bits, unsigned")
+    B, T, V, code, sampled_out, accept_len, num_emitted, emitted, workspace, ws_have = \
+        _accept_buffers(logits, q_start, sampled_out, accept_len, num_emitted, emitted, workspace)
+    rc = library().verify_accept_sampled(
+        B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
+        _dev_ptr(q_start, "q_start", i32), float(temperature), int(seed), int(offset),
+        _dev_ptr(sampled_out, "sampled_out", i32), _dev_ptr(accept_len, "accept_len", i32),
+        _dev_ptr(num_emitted, "num_emitted", i32), _dev_ptr(emitted, "emitted", i32),
+        _dev_ptr(workspace, "workspace"), ws_have, _stream_ptr(stream, logits.device))
+    _check(rc, "verify_accept_sampled")
+    return accept_len, num_emitted, emitted, sampled_out
 
 
 def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float, g_min: float,

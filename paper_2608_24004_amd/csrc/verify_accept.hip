@@ -8,6 +8,9 @@
 //                  chunk of one logits row with 16-byte coalesced loads and
 //                  reduces it to a packed (order key, ~index) 64-bit maximum,
 //                  which is the lowest index among equal maxima;
+//   sample_chunks  the same for stochastic verification: the maximum of the
+//                  logits over T plus Gumbel noise (a sample of the row's
+//                  softmax);
 //   accept_scan    one wavefront per request: reduces its rows' chunk
 //                  partials to the row argmax, then finds the first draft
 //                  that disagrees (wavefront ballot) and writes the accepted
@@ -159,6 +162,248 @@ __global__ __launch_bounds__(kArgmaxThreads) void argmax_chunks(
     }
 }
 
+// ---------------------------------------------------------------- sampling (T > 0)
+//
+// With drafts that put all their probability on one token, speculative
+// rejection sampling at temperature T accepts draft d with probability p(d)
+// and otherwise draws from p without d; drawing y ~ p = softmax(logits / T)
+// per row and accepting iff y == d is that same rule.  y is drawn by the
+// Gumbel-max rule y = argmax_v (x_v / T + g_v), g_v = -log(-log u_v), with u_v
+// from Philox4x32-10 (Salmon et al., SC 2011; key = seed, counter =
+// (v / 4, row, offset, 0), output word v % 4) and the log written below from
+// the atanh series, every step an fp32 operation with fixed rounding, so the
+// draw is reproducible bit for bit.  u = ((w >> 9) + 0.5) 2^-23 takes the top
+// 23 bits: an odd multiple of 2^-24 that fp32 holds exactly, inside
+// [2^-24, 1 - 2^-24], so g stays below 16.7 (24 bits would round the top code
+// to u = 1).
+//
+// sample_chunks has argmax_chunks' grid and output, but its cost is
+// arithmetic (the generator and two logs per logit), so it skips the logs of
+// logits that cannot win.  -log(-log u) <= -log(1 - u), and 1 - u = n 2^-24
+// with n = 2^24 - 2k - 1 (k = w >> 9), so g <= (clz(n) - 7) ln 2: a bound
+// from one integer instruction.  A logit whose score under that bound stays
+// below a score already reached in the chunk can be neither the row's maximum
+// nor tied with it.  The others are queued per wavefront in LDS and evaluated
+// 64 at a time, one per lane, so the logs run on full wavefronts.  The
+// threshold is the wavefront's best evaluated score, raised after every
+// batch; after the first batches almost no logit is queued.
+struct SampleParams {
+    uint32_t k0, k1;   // seed: key words
+    uint32_t offset;   // counter word 2 (e.g. the decoding step)
+    float inv_t;       // 1 / T, rounded to fp32 on the host
+};
+
+__device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                              uint32_t k0, uint32_t k1, uint32_t out[4]) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        // one 32 x 32 -> 64-bit product gives both halves of each multiply
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        c0 = n0;
+        c1 = (uint32_t)p1;
+        c2 = n2;
+        c3 = (uint32_t)p0;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}
+
+// log x for normal x > 0: x = m 2^e, m in [sqrt(1/2), sqrt(2)), z = (m-1)/(m+1),
+// log x = e ln 2 + 2 (z + z^3/3 + z^5/5 + z^7/7 + z^9/9).
+__device__ __forceinline__ float series_log(float x) {
+    const uint32_t bits = __float_as_uint(x);
+    int e = (int)((bits >> 23) & 0xFFu) - 127;
+    float m = __uint_as_float((bits & 0x7FFFFFu) | 0x3F800000u);
+    if (m > 1.41421354f) {
+        m = m * 0.5f;
+        e += 1;
+    }
+    const float z = (m - 1.0f) / (m + 1.0f);
+    const float z2 = z * z;
+    float poly = fmaf(z2, 0.111111112f, 0.142857149f);
+    poly = fmaf(z2, poly, 0.200000003f);
+    poly = fmaf(z2, poly, 0.333333343f);
+    poly = fmaf(z2, poly, 1.0f);
+    const float r = 2.0f * z * poly;
+    return fmaf((float)e, 0.693147182f, r);
+}
+
+// Gumbel noise of the 23-bit code k = w >> 9.
+__device__ __forceinline__ float gumbel_of_code(uint32_t k) {
+    const float u = ((float)k + 0.5f) * 0x1p-23f;
+    return -series_log(-series_log(u));
+}
+
+// An upper bound of gumbel_of_code(k): (clz(n) - 7) ln 2 >= -log(1 - u) >= g,
+// with ln 2 rounded up and 1e-3 added, far above the few 1e-6 by which the
+// fp32 evaluation of g can exceed its exact value.
+__device__ __forceinline__ float gumbel_bound(uint32_t k) {
+    const uint32_t n = 0xFFFFFFu - 2u * k;  // >= 1
+    return fmaf((float)(__clz(n) - 7), 0.69315f, 1.0e-3f);
+}
+constexpr float kGumbelMax = 16.64f;  // >= gumbel_bound(k) for every k (n = 1: 24 ln 2)
+
+constexpr int kSampleQueue = 2 * kWave;  // entries per wavefront queue
+constexpr int kSampleUnroll = 2;         // 16-byte vectors per lane per iteration
+
+template <typename T>
+__global__ __launch_bounds__(kArgmaxThreads) void sample_chunks(
+    const T* __restrict__ logits, int64_t row_stride, int64_t vocab, int64_t chunk_elems,
+    int nchunks, uint64_t* __restrict__ partial, SampleParams sp) {
+    constexpr int E = Storage<T>::kPer16B;
+    // queued logit: (x bits, code k, index, unused)
+    __shared__ uint4 queue[kArgmaxThreads / kWave][kSampleQueue];
+    __shared__ uint64_t red[kArgmaxThreads / kWave];
+    const int64_t row = blockIdx.y;
+    const uint32_t urow = (uint32_t)row;
+    const int c = blockIdx.x;
+    const T* rowp = logits + row * row_stride;
+    const int64_t lo = (int64_t)c * chunk_elems;
+    const int64_t hi = min(vocab, lo + chunk_elems);
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wid = tid / kWave;
+    uint4* q = queue[wid];
+
+    float best = -INFINITY;     // best evaluated score of this lane ...
+    uint32_t best_idx = kNone;  // ... and its index (lowest among equal scores)
+    uint32_t nan_idx = kNone;   // first NaN seen
+    float thr = -INFINITY;      // wavefront-uniform: a score reached in this chunk
+    int qn = 0;                 // wavefront-uniform queue fill
+
+    auto take = [&](float x, uint32_t k, uint32_t idx) {
+        const float s = fmaf(x, sp.inv_t, gumbel_of_code(k));
+        if (s > best || (s == best && idx < best_idx)) {
+            best = s;
+            best_idx = idx;
+        }
+    };
+    // Evaluate queue entries 0..63 (one per lane) and move the rest down.  One
+    // wavefront's LDS accesses are served in program order, and the moved
+    // entries [64, qn) never overlap their targets [0, qn - 64).
+    auto flush = [&]() {
+        const uint4 e = q[lane];
+        const int rest = qn - kWave;
+        uint4 m = make_uint4(0u, 0u, 0u, 0u);
+        if (lane < rest) m = q[kWave + lane];
+        asm volatile("" ::: "memory");
+        if (lane < rest) q[lane] = m;
+        asm volatile("" ::: "memory");
+        take(__uint_as_float(e.x), e.y, e.z);
+        qn = rest;
+        const float wm = wave_max_xor(best, kWave);
+        thr = fmaxf(thr, __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(wm))));
+    };
+    // One 16-byte vector of E logits at element `base`; `have` is false for
+    // lanes past the chunk's last vector, which still take part in the ballots.
+    auto scan = [&](const uint4& v, uint32_t base, bool have) {
+        float x[E];
+        unpack16(v, x, T());
+        const bool nan = have && ((E == 8) ? any_nan_bf16x8(v) : any_nan_f32x4(v));
+        if (nan && nan_idx == kNone) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                if (x[e] != x[e]) { nan_idx = base + e; break; }
+            }
+        }
+        // a lane that holds a NaN reports it; its other logits drop out
+        const bool live = have && nan_idx == kNone;
+#pragma unroll
+        for (int b = 0; b < E / 4; ++b) {
+            const float xm = fmaxf(fmaxf(x[4 * b], x[4 * b + 1]), fmaxf(x[4 * b + 2], x[4 * b + 3]));
+            const bool any = live && fmaf(xm, sp.inv_t, kGumbelMax) >= thr;
+            if (__ballot(any) == 0) continue;
+            uint32_t w[4];
+            philox4x32_10((base >> 2) + b, urow, sp.offset, 0u, sp.k0, sp.k1, w);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t k = w[e] >> 9;
+                const float xe = x[4 * b + e];
+                const bool cand = any && fmaf(xe, sp.inv_t, gumbel_bound(k)) >= thr;
+                const uint64_t bal = __ballot(cand);
+                if (bal == 0) continue;
+                if (cand) {
+                    const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                        (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+                    q[qn + (int)below] = make_uint4(__float_as_uint(xe), k, base + 4 * b + e, 0u);
+                }
+                qn += (int)__popcll(bal);
+                if (qn >= kWave) flush();
+            }
+        }
+    };
+    // A logit outside the 16-byte vectors, evaluated directly (ascending per lane).
+    auto one = [&](int64_t e) {
+        const float x = Storage<T>::load(rowp, e);
+        if (x != x) {
+            if (nan_idx == kNone) nan_idx = (uint32_t)e;
+        } else if (nan_idx == kNone) {
+            uint32_t w[4];
+            philox4x32_10((uint32_t)(e >> 2), urow, sp.offset, 0u, sp.k0, sp.k1, w);
+            take(x, w[e & 3] >> 9, (uint32_t)e);
+        }
+    };
+
+    if ((reinterpret_cast<uintptr_t>(rowp + lo) & 15u) == 0) {
+        const uint4* vp = reinterpret_cast<const uint4*>(rowp + lo);
+        const int64_t nvec = (hi - lo) / E;
+        // Loop bounds are per wavefront (every lane reaches every ballot);
+        // the next iteration's vectors load while this one's are scanned.
+        constexpr int64_t kStep = (int64_t)kSampleUnroll * kArgmaxThreads;
+        const int64_t wave_first = tid - lane;
+        uint4 cur[kSampleUnroll], nxt[kSampleUnroll];
+        auto load = [&](int64_t v0, uint4 (&dst)[kSampleUnroll]) {
+#pragma unroll
+            for (int u = 0; u < kSampleUnroll; ++u) {
+                const int64_t vi = v0 + u * kArgmaxThreads + tid;
+                dst[u] = vi < nvec ? ld16_stream(vp + vi) : make_uint4(0u, 0u, 0u, 0u);
+            }
+        };
+        if (wave_first < nvec) load(0, cur);
+        for (int64_t v0 = 0; v0 + wave_first < nvec; v0 += kStep) {
+            if (v0 + kStep + wave_first < nvec) load(v0 + kStep, nxt);
+#pragma unroll
+            for (int u = 0; u < kSampleUnroll; ++u) {
+                const int64_t vi = v0 + u * kArgmaxThreads + tid;
+                scan(cur[u], (uint32_t)(lo + vi * E), vi < nvec);
+            }
+#pragma unroll
+            for (int u = 0; u < kSampleUnroll; ++u) cur[u] = nxt[u];
+        }
+        for (int64_t e = lo + nvec * E + tid; e < hi; e += kArgmaxThreads) one(e);
+    } else {
+        for (int64_t e = lo + tid; e < hi; e += kArgmaxThreads) one(e);
+    }
+    if (qn > 0 && lane < qn) {
+        const uint4 e = q[lane];
+        take(__uint_as_float(e.x), e.y, e.z);
+    }
+
+    uint64_t packed = 0;
+    if (nan_idx != kNone) {
+        packed = pack(0xffffffffu, nan_idx);
+    } else if (best_idx != kNone) {
+        packed = pack(order_key(__float_as_uint(best)), best_idx);
+    }
+    packed = wave_max_u64(packed);
+    if (lane == 0) red[wid] = packed;
+    __syncthreads();
+    if (tid == 0) {
+        uint64_t m = red[0];
+#pragma unroll
+        for (int w = 1; w < kArgmaxThreads / kWave; ++w) m = red[w] > m ? red[w] : m;
+        partial[row * nchunks + c] = m;
+    }
+}
+
 __global__ __launch_bounds__(kWave) void accept_scan(
     int num_seqs, const int32_t* __restrict__ q_start, const int32_t* __restrict__ tokens,
     const uint64_t* __restrict__ partial, int nchunks, int32_t* __restrict__ argmax_out,
@@ -239,6 +484,54 @@ bool accept_args_ok(int32_t num_seqs, int32_t total_q, int64_t vocab, int32_t dt
            (dtype == VERIFY_F32 || dtype == VERIFY_BF16);
 }
 
+// Launch the per-chunk scan (argmax, or the sampler when sp is given) and the
+// acceptance scan after argument checks shared by both entry points.
+int accept_launch(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_stride,
+                  int32_t logits_dtype, const void* logits, const int32_t* tokens,
+                  const int32_t* q_start, int32_t* argmax_out, int32_t* accept_len,
+                  int32_t* num_emitted, int32_t* emitted, void* workspace, size_t workspace_bytes,
+                  const SampleParams* sp, hipStream_t stream) {
+    if (logits_dtype != VERIFY_F32 && logits_dtype != VERIFY_BF16) return VERIFY_EUNSUPPORTED;
+    if (!accept_args_ok(num_seqs, total_q, vocab, logits_dtype)) return VERIFY_EINVAL;
+    if (row_stride == 0) row_stride = vocab;
+    if (row_stride < vocab) return VERIFY_EINVAL;
+    if (num_seqs > 0 && (!q_start || !accept_len || !num_emitted)) return VERIFY_EINVAL;
+    if (total_q > 0 && (!logits || !tokens || !emitted)) return VERIFY_EINVAL;
+    const AcceptPlan p = plan_accept(total_q, vocab, logits_dtype);
+    const size_t need = p.partial_bytes + p.argmax_bytes;
+    if (workspace_bytes < need || (need > 0 && !workspace)) return VERIFY_EWORKSPACE;
+    if (num_seqs == 0) return VERIFY_OK;
+
+    uint64_t* partial = static_cast<uint64_t*>(workspace);
+    int32_t* am = argmax_out ? argmax_out
+                             : reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + p.partial_bytes);
+    if (total_q > 0) {
+        dim3 grid(p.nchunks, total_q), block(kArgmaxThreads);
+        const bool bf16 = logits_dtype == VERIFY_BF16;
+        if (sp && bf16) {
+            hipLaunchKernelGGL(sample_chunks<uint16_t>, grid, block, 0, stream,
+                               static_cast<const uint16_t*>(logits), row_stride, vocab,
+                               p.chunk_elems, p.nchunks, partial, *sp);
+        } else if (sp) {
+            hipLaunchKernelGGL(sample_chunks<float>, grid, block, 0, stream,
+                               static_cast<const float*>(logits), row_stride, vocab,
+                               p.chunk_elems, p.nchunks, partial, *sp);
+        } else if (bf16) {
+            hipLaunchKernelGGL(argmax_chunks<uint16_t>, grid, block, 0, stream,
+                               static_cast<const uint16_t*>(logits), row_stride, vocab,
+                               p.chunk_elems, p.nchunks, partial);
+        } else {
+            hipLaunchKernelGGL(argmax_chunks<float>, grid, block, 0, stream,
+                               static_cast<const float*>(logits), row_stride, vocab,
+                               p.chunk_elems, p.nchunks, partial);
+        }
+        if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
+    }
+    hipLaunchKernelGGL(accept_scan, dim3(num_seqs), dim3(kWave), 0, stream, num_seqs, q_start,
+                       tokens, partial, p.nchunks, am, accept_len, num_emitted, emitted);
+    return check_launch();
+}
+
 }  // namespace
 }  // namespace averify
 
@@ -261,34 +554,26 @@ extern "C" int verify_accept(int32_t num_seqs, int32_t total_q, int64_t vocab, i
                              const int32_t* q_start, int32_t* argmax_out, int32_t* accept_len,
                              int32_t* num_emitted, int32_t* emitted, void* workspace,
                              size_t workspace_bytes, hipStream_t stream) {
-    if (logits_dtype != VERIFY_F32 && logits_dtype != VERIFY_BF16) return VERIFY_EUNSUPPORTED;
-    if (!accept_args_ok(num_seqs, total_q, vocab, logits_dtype)) return VERIFY_EINVAL;
-    if (row_stride == 0) row_stride = vocab;
-    if (row_stride < vocab) return VERIFY_EINVAL;
-    if (num_seqs > 0 && (!q_start || !accept_len || !num_emitted)) return VERIFY_EINVAL;
-    if (total_q > 0 && (!logits || !tokens || !emitted)) return VERIFY_EINVAL;
-    const AcceptPlan p = plan_accept(total_q, vocab, logits_dtype);
-    const size_t need = p.partial_bytes + p.argmax_bytes;
-    if (workspace_bytes < need || (need > 0 && !workspace)) return VERIFY_EWORKSPACE;
-    if (num_seqs == 0) return VERIFY_OK;
+    return accept_launch(num_seqs, total_q, vocab, row_stride, logits_dtype, logits, tokens, q_start,
+                         argmax_out, accept_len, num_emitted, emitted, workspace, workspace_bytes,
+                         nullptr, stream);
+}
 
-    uint64_t* partial = static_cast<uint64_t*>(workspace);
-    int32_t* am = argmax_out ? argmax_out
-                             : reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + p.partial_bytes);
-    if (total_q > 0) {
-        dim3 grid(p.nchunks, total_q);
-        if (logits_dtype == VERIFY_BF16) {
-            hipLaunchKernelGGL(argmax_chunks<uint16_t>, grid, dim3(kArgmaxThreads), 0, stream,
-                               static_cast<const uint16_t*>(logits), row_stride, vocab,
-                               p.chunk_elems, p.nchunks, partial);
-        } else {
-            hipLaunchKernelGGL(argmax_chunks<float>, grid, dim3(kArgmaxThreads), 0, stream,
-                               static_cast<const float*>(logits), row_stride, vocab,
-                               p.chunk_elems, p.nchunks, partial);
-        }
-        if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
-    }
-    hipLaunchKernelGGL(accept_scan, dim3(num_seqs), dim3(kWave), 0, stream, num_seqs, q_start,
-                       tokens, partial, p.nchunks, am, accept_len, num_emitted, emitted);
-    return check_launch();
+extern "C" int verify_accept_sampled(int32_t num_seqs, int32_t total_q, int64_t vocab,
+                                     int64_t row_stride, int32_t logits_dtype, const void* logits,
+                                     const int32_t* tokens, const int32_t* q_start,
+                                     float temperature, uint64_t seed, uint32_t offset,
+                                     int32_t* sampled_out, int32_t* accept_len, int32_t* num_emitted,
+                                     int32_t* emitted, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+    if (!(temperature > 0.0f) || !(temperature < 3.0e38f)) return VERIFY_EINVAL;
+    SampleParams sp;
+    sp.k0 = (uint32_t)seed;
+    sp.k1 = (uint32_t)(seed >> 32);
+    sp.offset = offset;
+    sp.inv_t = (float)(1.0 / (double)temperature);
+    if (!(sp.inv_t > 0.0f) || !(sp.inv_t < 3.0e38f)) return VERIFY_EINVAL;
+    return accept_launch(num_seqs, total_q, vocab, row_stride, logits_dtype, logits, tokens, q_start,
+                         sampled_out, accept_len, num_emitted, emitted, workspace, workspace_bytes,
+                         &sp, stream);
 }

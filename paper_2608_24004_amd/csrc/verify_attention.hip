@@ -1340,4 +1340,4 @@ extern "C" const char* verify_status_string(int status) {
     }
 }
 
-extern "C" int verify_abi_version(void) { return 10100; }
+extern "C" int verify_abi_version(void) { return 10200; }

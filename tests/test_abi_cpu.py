@@ -26,7 +26,8 @@ def declared_symbols():
 
 def test_header_declares_the_entry_points():
     names = declared_symbols()
-    for n in ("verify_attention", "verify_accept", "verify_attention_workspace_size",
+    for n in ("verify_attention", "verify_accept", "verify_accept_sampled", "verify_budget",
+              "verify_kv_append", "verify_attention_workspace_size",
               "verify_accept_workspace_size", "verify_status_string", "verify_abi_version"):
         assert n in names
 
@@ -35,7 +36,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10100
+    assert av.abi_version() == 10200
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
@@ -140,6 +141,30 @@ def test_accept_argument_validation():
     assert lib.verify_accept(4, 40, 100, 0, av.F32, *args, dummy, n.value - 1, None) == av.EWORKSPACE
     # empty batch is a no-op
     assert lib.verify_accept(0, 0, 100, 0, av.F32, *([None] * 8), 0, None) == 0
+
+
+def test_accept_sampled_argument_validation():
+    lib = av.library()
+    n = ctypes.c_size_t(0)
+    lib.verify_accept_workspace_size(4, 40, 100, av.F32, ctypes.byref(n))
+    d = ctypes.c_void_p(0x1000)
+
+    def call(temperature=1.0, stride=0, dtype=av.F32, ws=n.value, accept=d, logits=d):
+        return lib.verify_accept_sampled(4, 40, 100, stride, dtype, logits, d, d, temperature,
+                                         (1 << 64) - 1, (1 << 32) - 1, None, accept, d, d, d, ws,
+                                         None)
+
+    for t in (0.0, -1.0, float("nan"), float("inf"), 1e-45):   # 1e-45: 1/T overflows fp32
+        assert call(temperature=t) == av.EINVAL, t
+    assert call(stride=50) == av.EINVAL
+    assert call(accept=None) == av.EINVAL
+    assert call(logits=None) == av.EINVAL
+    assert call(dtype=9) == av.EUNSUPPORTED
+    assert call(ws=n.value - 1) == av.EWORKSPACE
+    assert lib.verify_accept_sampled(0, 0, 100, 0, av.F32, *([None] * 3), 0.7, 1, 0,
+                                     *([None] * 5), 0, None) == 0
+    with pytest.raises(ValueError):
+        av.verify_accept_sampled(None, None, None, temperature=1.0, seed=-1)
 
 
 def test_budget_argument_validation():
