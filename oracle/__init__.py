@@ -65,6 +65,8 @@ def _load():
     lib.oracle_attention.restype = ctypes.c_int
     lib.oracle_argmax.argtypes = [i64, i64, i64, i32, vp, vp, vp]
     lib.oracle_argmax.restype = ctypes.c_int
+    lib.oracle_lmhead_argmax.argtypes = [i64, vp, i32, i64, i32, vp, vp, vp, vp, vp]
+    lib.oracle_lmhead_argmax.restype = ctypes.c_int
     lib.oracle_accept.argtypes = [i32, vp, vp, vp, vp, vp, vp]
     lib.oracle_accept.restype = ctypes.c_int
     lib.oracle_budget.argtypes = [i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp, vp,
@@ -178,6 +180,31 @@ def argmax(logits, dtype: int, with_gap: bool = True):
     if rc != 0:
         raise ValueError("oracle_argmax rejected its arguments")
     return am, gap
+
+
+def lmhead_argmax(hidden_states, weight, dtype: int, rows=None, with_logits: bool = False):
+    """Argmax (and gap to the runner-up) of the logits <hidden[r], weight[v]>
+    for the selected rows (all if None), computed in double from the
+    storage arrays hidden_states [T, H] and weight [V, H].  Returns
+    (argmax, gap) or (argmax, gap, logits [n, V]) with with_logits."""
+    lib = _load()
+    hs = _raw(hidden_states, dtype)
+    w = _raw(weight, dtype)
+    T, H = hs.shape
+    V, H2 = w.shape
+    if H != H2:
+        raise ValueError("hidden sizes differ: %d vs %d" % (H, H2))
+    sel = np.arange(T, dtype=np.int32) if rows is None else np.ascontiguousarray(rows, dtype=np.int32)
+    if sel.size and (sel.min() < 0 or sel.max() >= T):
+        raise ValueError("selected row out of range")
+    am = np.zeros(sel.size, dtype=np.int32)
+    gap = np.zeros(sel.size, dtype=np.float64)
+    lg = np.zeros((sel.size, V), dtype=np.float64) if with_logits else None
+    rc = lib.oracle_lmhead_argmax(sel.size, _ptr(sel), H, V, dtype, _ptr(hs), _ptr(w), _ptr(am),
+                                  _ptr(gap), _ptr(lg) if with_logits else None)
+    if rc != 0:
+        raise ValueError("oracle_lmhead_argmax rejected its arguments")
+    return (am, gap, lg) if with_logits else (am, gap)
 
 
 def inv_temperature(temperature: float) -> np.float32:

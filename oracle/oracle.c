@@ -19,6 +19,9 @@
  *   oracle_kv_append  -- the new tokens' K/V written into their cache slots.
  *   oracle_argmax     -- per logits row, the lowest index attaining the maximum
  *                        (plus the gap to the runner-up, for near-tie flags).
+ *   oracle_lmhead_argmax -- the logits of selected rows from the final hidden
+ *                        states and the LM-head weight (a plain dot product
+ *                        per vocabulary entry), then oracle_argmax's rule.
  *   oracle_sample     -- each row's token drawn from softmax(logits / T) by the
  *                        Gumbel-max rule (Philox4x32-10 noise), the stochastic
  *                        verification's replacement for the argmax.
@@ -190,6 +193,52 @@ int oracle_argmax(int64_t rows, int64_t vocab, int64_t row_stride, int32_t dtype
             gap[r] = vocab == 1 ? INFINITY : bestv - second;
         }
     }
+    return 0;
+}
+
+/*
+ * The verify pass ends with the LM head: logits[r][v] = <hidden[r], weight[v]>,
+ * hidden [rows][H] and weight [vocab][H] (the usual lm_head layout), both in
+ * `dtype`.  The products of the exact inputs are summed in double, h
+ * ascending, and the row's argmax follows oracle_argmax (lowest index among
+ * equal maxima, the first NaN if any, -0.0 == +0.0), with the gap to the
+ * runner-up (NaN for a NaN row, +inf when vocab = 1).  Only the n_sel rows
+ * listed in sel_rows are computed; argmax, gap and (if not NULL) logits
+ * [n_sel][vocab] receive them in that order.  Returns 0, or -1 on bad sizes.
+ */
+int oracle_lmhead_argmax(int64_t n_sel, const int32_t *sel_rows, int32_t hidden, int64_t vocab,
+                         int32_t dtype, const void *hid, const void *weight, int32_t *argmax,
+                         double *gap, double *logits)
+{
+    if (vocab <= 0 || hidden <= 0) return -1;
+    double *row = (double *)malloc(sizeof(double) * vocab);
+    if (!row) return -1;
+    for (int64_t s = 0; s < n_sel; ++s) {
+        const int64_t r = sel_rows[s];
+#pragma omp parallel for schedule(static)
+        for (int64_t v = 0; v < vocab; ++v) {
+            double acc = 0.0;
+            for (int32_t h = 0; h < hidden; ++h)
+                acc += elem_to_double(hid, dtype, r * hidden + h) *
+                       elem_to_double(weight, dtype, v * hidden + h);
+            row[v] = acc;
+        }
+        int64_t best = 0;
+        int has_nan = isnan(row[0]);
+        for (int64_t v = 1; v < vocab && !has_nan; ++v) {
+            if (isnan(row[v])) { best = v; has_nan = 1; }
+            else if (row[v] > row[best]) best = v;
+        }
+        argmax[s] = (int32_t)best;
+        if (gap) {
+            double second = -INFINITY;
+            for (int64_t v = 0; v < vocab; ++v)
+                if (v != best && row[v] > second) second = row[v];
+            gap[s] = has_nan ? NAN : (vocab == 1 ? INFINITY : row[best] - second);
+        }
+        if (logits) memcpy(logits + s * vocab, row, sizeof(double) * vocab);
+    }
+    free(row);
     return 0;
 }
 

@@ -1328,16 +1328,3 @@ extern "C" int verify_kv_append(const verify_attn_params* params, int32_t total_
 #undef AVERIFY_APPEND
     return check_launch();
 }
-
-extern "C" const char* verify_status_string(int status) {
-    switch (status) {
-        case VERIFY_OK: return "ok";
-        case VERIFY_EINVAL: return "invalid argument";
-        case VERIFY_EUNSUPPORTED: return "unsupported shape or dtype";
-        case VERIFY_EWORKSPACE: return "workspace too small";
-        case VERIFY_EHIP: return "HIP launch failure";
-        default: return "unknown status";
-    }
-}
-
-extern "C" int verify_abi_version(void) { return 10200; }
