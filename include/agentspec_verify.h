@@ -26,6 +26,10 @@
  *                       draws its token from softmax(logits / T) instead of
  *                       taking the argmax (speculative sampling with drafts
  *                       that are single tokens).
+ *   verify_lmhead_accept -- verify_accept fed by the LM head itself: the
+ *                       logits of every scored position are computed from the
+ *                       final hidden states and reduced to the argmax on the
+ *                       fly, never stored.
  *
  * Conventions shared by both calls
  * --------------------------------
@@ -218,6 +222,42 @@ int verify_accept_sampled(int32_t num_seqs, int32_t total_q, int64_t vocab, int6
                           uint32_t offset, int32_t *sampled_out, int32_t *accept_len,
                           int32_t *num_emitted, int32_t *emitted, void *workspace,
                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * verify_lmhead_accept -- the verify pass's LM head fused with greedy
+ * acceptance (Sec. 2.2: the target scores every proposed position in one pass
+ * and keeps the drafts that agree with its own greedy choice).
+ *
+ * For every scored row r and vocabulary entry v the logit is
+ *     z[r][v] = <hidden[r], weight[v]>        (bf16 products, fp32 sums)
+ * and argmax[r] is the lowest v attaining the row maximum (a NaN logit counts
+ * as the maximum: the first NaN wins; -0.0 equals +0.0).  The logits are
+ * reduced as they are produced and never written to memory.  Acceptance then
+ * follows verify_accept exactly.  The fp32 sums are taken in a fixed order
+ * inside the kernel but not in ascending h, so two logits closer than the
+ * rounding of a hidden_size-term fp32 dot product may compare either way;
+ * the plain definition in exact arithmetic fixes the order otherwise.
+ *
+ *   hidden      [total_q][hidden_size] bf16: the final hidden states (after
+ *               the last normalisation) of the scored rows
+ *   weight      [vocab][hidden_size] bf16: the LM-head (output embedding)
+ *               weight, row v = token v
+ *   hidden_size multiple of 32; vocab >= 1 and < 2^31; both pointers 16-byte
+ *               aligned (VERIFY_EINVAL otherwise)
+ *   dtype       VERIFY_BF16 (VERIFY_F32 returns VERIFY_EUNSUPPORTED)
+ * tokens, q_start, argmax_out, accept_len, num_emitted and emitted are
+ * verify_accept's.  workspace: at least
+ * verify_lmhead_accept_workspace_size() bytes (may be NULL if that is 0); its
+ * contents on entry are ignored.
+ */
+int verify_lmhead_accept_workspace_size(int32_t num_seqs, int32_t total_q, int32_t hidden_size,
+                                        int64_t vocab, int32_t dtype, size_t *bytes);
+
+int verify_lmhead_accept(int32_t num_seqs, int32_t total_q, int32_t hidden_size, int64_t vocab,
+                         int32_t dtype, const void *hidden, const void *weight,
+                         const int32_t *tokens, const int32_t *q_start, int32_t *argmax_out,
+                         int32_t *accept_len, int32_t *num_emitted, int32_t *emitted,
+                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * verify_budget -- redundancy-aware draft budget (Sec. 4.2, Alg. 2).

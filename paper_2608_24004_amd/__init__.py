@@ -5,8 +5,11 @@ marshalling only.  Every step of the verify pass runs in the HIP kernels of
 ``libagentspec_verify.so``; PyTorch supplies device memory and the stream.
 If the library is missing, every entry point raises -- there is no fallback.
 
-    verify_attention(...)  paged multi-query GQA attention of all scored rows
-    verify_accept(...)     vocabulary argmax + greedy acceptance of the drafts
+    verify_attention(...)      paged multi-query GQA attention of all scored rows
+    verify_accept(...)         vocabulary argmax + greedy acceptance of the drafts
+    verify_lmhead_accept(...)  the same acceptance fed by the LM head, logits
+                               never stored
+    verify_accept_sampled(...), verify_budget(...), verify_kv_append(...)
 """
 from __future__ import annotations
 
@@ -16,8 +19,9 @@ from typing import Optional
 
 from .build import LIB_PATH
 
-__all__ = ["verify_attention", "verify_accept", "attention_workspace_size",
-           "accept_workspace_size", "VerifyError", "library", "abi_version", "F32", "BF16"]
+__all__ = ["verify_attention", "verify_accept", "verify_accept_sampled", "verify_lmhead_accept",
+           "verify_budget", "verify_kv_append", "attention_workspace_size", "accept_workspace_size",
+           "lmhead_accept_workspace_size", "VerifyError", "library", "abi_version", "F32", "BF16"]
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
@@ -74,6 +78,11 @@ def library(path: Optional[str] = None):
                                           ctypes.c_uint64, ctypes.c_uint32, vp, vp, vp, vp, vp, sz, vp]
     lib.verify_accept_sampled.restype = ctypes.c_int
     f64 = ctypes.c_double
+    lib.verify_lmhead_accept_workspace_size.argtypes = [i32, i32, i32, i64, i32, ctypes.POINTER(sz)]
+    lib.verify_lmhead_accept_workspace_size.restype = ctypes.c_int
+    lib.verify_lmhead_accept.argtypes = [i32, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                         sz, vp]
+    lib.verify_lmhead_accept.restype = ctypes.c_int
     lib.verify_budget.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp,
                                   vp, i64, vp, vp]
     lib.verify_budget.restype = ctypes.c_int
@@ -267,6 +276,56 @@ def verify_accept_sampled(logits, tokens, q_start, *, temperature: float, seed: 
         _dev_ptr(workspace, "workspace"), ws_have, _stream_ptr(stream, logits.device))
     _check(rc, "verify_accept_sampled")
     return accept_len, num_emitted, emitted, sampled_out
+
+
+def lmhead_accept_workspace_size(num_seqs: int, total_q: int, hidden_size: int, vocab: int,
+                                 dtype_code: int = BF16) -> int:
+    n = ctypes.c_size_t(0)
+    _check(library().verify_lmhead_accept_workspace_size(int(num_seqs), int(total_q), int(hidden_size),
+                                                         int(vocab), int(dtype_code), ctypes.byref(n)),
+           "verify_lmhead_accept_workspace_size")
+    return int(n.value)
+
+
+def verify_lmhead_accept(hidden, weight, tokens, q_start, *, argmax_out=None, accept_len=None,
+                         num_emitted=None, emitted=None, workspace=None, stream=None):
+    """LM head fused with greedy acceptance: logits <hidden[r], weight[v]> are
+    reduced to each row's argmax inside the kernel (never stored), then the
+    drafts are accepted as in verify_accept.
+
+    hidden [T, H] and weight [V, H] bf16, tokens [T] and q_start [B+1] int32,
+    all on the device.  Returns (accept_len [B], num_emitted [B], emitted [T],
+    argmax [T]).
+    """
+    import torch
+    i32 = torch.int32
+    T, H = hidden.shape
+    V, H2 = weight.shape
+    if H != H2:
+        raise ValueError("hidden sizes differ: %d vs %d" % (H, H2))
+    B = q_start.shape[0] - 1
+    dev = hidden.device
+    code = _dtype_code(hidden)
+    if argmax_out is None:
+        argmax_out = torch.empty(T, dtype=i32, device=dev)
+    if accept_len is None:
+        accept_len = torch.empty(B, dtype=i32, device=dev)
+    if num_emitted is None:
+        num_emitted = torch.empty(B, dtype=i32, device=dev)
+    if emitted is None:
+        emitted = torch.empty(T, dtype=i32, device=dev)
+    ws_bytes = lmhead_accept_workspace_size(B, T, H, V, code)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_have = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    rc = library().verify_lmhead_accept(
+        B, T, H, V, code, _dev_ptr(hidden, "hidden"), _dev_ptr(weight, "weight", hidden.dtype),
+        _dev_ptr(tokens, "tokens", i32), _dev_ptr(q_start, "q_start", i32),
+        _dev_ptr(argmax_out, "argmax_out", i32), _dev_ptr(accept_len, "accept_len", i32),
+        _dev_ptr(num_emitted, "num_emitted", i32), _dev_ptr(emitted, "emitted", i32),
+        _dev_ptr(workspace, "workspace"), ws_have, _stream_ptr(stream, dev))
+    _check(rc, "verify_lmhead_accept")
+    return accept_len, num_emitted, emitted, argmax_out
 
 
 def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float, g_min: float,

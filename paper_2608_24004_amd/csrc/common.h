@@ -92,7 +92,65 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     return v;
 }
 
+// ---------------------------------------------------------------- argmax keys
+
+// Monotone map from a float to an unsigned key: a > b  <=>  key(a) > key(b)
+// for non-NaN values, -0.0 and +0.0 share a key, and NaN maps above +inf.
+__device__ __forceinline__ uint32_t order_key(uint32_t bits) {
+    const uint32_t mag = bits & 0x7fffffffu;
+    if (mag > 0x7f800000u) return 0xffffffffu;
+    if (mag == 0) bits = 0;
+    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+
+// (order key, ~index) in one word: the larger word has the larger key and,
+// among equal keys, the lower index, so a max-reduction keeps the first maximum.
+__device__ __forceinline__ uint64_t pack(uint32_t key, uint32_t idx) {
+    return ((uint64_t)key << 32) | (uint32_t)(0xffffffffu - idx);
+}
+
+// ---------------------------------------------------------------- global->LDS pipelines
+
+// s_waitcnt immediate (gfx9 encoding) that waits for vmcnt == 0 and leaves
+// expcnt (bits 6:4) and lgkmcnt (bits 11:8) at their no-wait maxima.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Workgroup barrier that orders LDS only: the staging rings live in LDS and
+// global memory needs no ordering between the waves of a workgroup.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// 16 bytes per lane from global memory straight into LDS (gfx950
+// global_load_lds_dwordx4): lane l of the wavefront writes LDS bytes
+// [lds + 16 l, lds + 16 l + 16).  The load is issued from inline assembly so
+// that its completion is tracked by the pipeline's explicit waits alone; the
+// compiler does not see it and adds no waits of its own.
+__device__ __forceinline__ void dma16(uint32_t lds_wave_base, const void* src) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_wave_base)), "v"(src)
+                 : "memory", "m0");
+}
+
+// Wait until at most N vector-memory operations of this wavefront are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
 // ---------------------------------------------------------------- host helpers
+
+// Greedy acceptance from per-(row, chunk) packed maxima (verify_accept.hip):
+// reduces partial[row * nchunks + c] over c to each row's argmax, then writes
+// the accepted drafts and the bonus token of every request.  Returns a status.
+int launch_accept_scan(int num_seqs, const int32_t* q_start, const int32_t* tokens,
+                       const uint64_t* partial, int nchunks, int32_t* argmax_out,
+                       int32_t* accept_len, int32_t* num_emitted, int32_t* emitted,
+                       hipStream_t stream);
 
 inline int check_launch() {
     return hipGetLastError() == hipSuccess ? VERIFY_OK : VERIFY_EHIP;

@@ -23,19 +23,6 @@ namespace {
 constexpr int kArgmaxThreads = 256;
 constexpr int kArgmaxUnroll = 4;  // 16-byte vectors in flight per thread
 
-// Monotone map from a float to an unsigned key: a > b  <=>  key(a) > key(b)
-// for non-NaN values, -0.0 and +0.0 share a key, and NaN maps above +inf.
-__device__ __forceinline__ uint32_t order_key(uint32_t bits) {
-    const uint32_t mag = bits & 0x7fffffffu;
-    if (mag > 0x7f800000u) return 0xffffffffu;
-    if (mag == 0) bits = 0;
-    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
-}
-
-__device__ __forceinline__ uint64_t pack(uint32_t key, uint32_t idx) {
-    return ((uint64_t)key << 32) | (uint32_t)(0xffffffffu - idx);
-}
-
 // True if any bf16 half of the four words is a NaN (|h| > 0x7f80).
 __device__ __forceinline__ bool any_nan_bf16x8(const uint4& v) {
     const uint32_t m = 0x7fff7fffu, c = 0x007f007fu, s = 0x80008000u;
@@ -527,12 +514,22 @@ int accept_launch(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_
         }
         if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
     }
-    hipLaunchKernelGGL(accept_scan, dim3(num_seqs), dim3(kWave), 0, stream, num_seqs, q_start,
-                       tokens, partial, p.nchunks, am, accept_len, num_emitted, emitted);
-    return check_launch();
+    return launch_accept_scan(num_seqs, q_start, tokens, partial, p.nchunks, am, accept_len,
+                              num_emitted, emitted, stream);
 }
 
 }  // namespace
+
+int launch_accept_scan(int num_seqs, const int32_t* q_start, const int32_t* tokens,
+                       const uint64_t* partial, int nchunks, int32_t* argmax_out,
+                       int32_t* accept_len, int32_t* num_emitted, int32_t* emitted,
+                       hipStream_t stream) {
+    if (num_seqs <= 0) return VERIFY_OK;
+    hipLaunchKernelGGL(accept_scan, dim3(num_seqs), dim3(kWave), 0, stream, num_seqs, q_start,
+                       tokens, partial, nchunks, argmax_out, accept_len, num_emitted, emitted);
+    return check_launch();
+}
+
 }  // namespace averify
 
 using namespace averify;

@@ -276,31 +276,6 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
 // running max and rescale factor live in the lanes that own its scores.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
-// s_waitcnt immediate (gfx9 encoding) that waits for vmcnt == 0 and leaves
-// expcnt (bits 6:4) and lgkmcnt (bits 11:8) at their no-wait maxima.
-constexpr int kWaitVmcnt0 = 0x0F70;
-
-// Workgroup barrier that orders LDS only: the KV ring lives in LDS and global
-// memory needs no ordering between the waves of a workgroup here.
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// 16 bytes per lane from global memory straight into LDS (gfx950
-// global_load_lds_dwordx4): lane l of the wavefront writes LDS bytes
-// [lds + 16 l, lds + 16 l + 16).  The load is issued from inline assembly so
-// that its completion is tracked by the explicit waits of the KV pipeline
-// alone; the compiler does not see it and adds no waits of its own.
-__device__ __forceinline__ void dma16(uint32_t lds_wave_base, const void* src) {
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :
-                 : "s"(__builtin_amdgcn_readfirstlane(lds_wave_base)), "v"(src)
-                 : "memory", "m0");
-}
-
-
 // Maximum of v over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes that hold
 // one row of an MFMA result tile).  Each permlane swap exchanges half of the
 // wavefront between its two operands; with both operands equal to v, the two
@@ -316,12 +291,6 @@ __device__ __forceinline__ float row_max_4lanes(float v) {
 // row maximum is raised.
 constexpr float kSlackLog2 = 8.f;
 
-// Wait until at most N vector-memory operations of this wavefront are in flight.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
-    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 

@@ -28,7 +28,8 @@ def test_header_declares_the_entry_points():
     names = declared_symbols()
     for n in ("verify_attention", "verify_accept", "verify_accept_sampled", "verify_budget",
               "verify_kv_append", "verify_attention_workspace_size",
-              "verify_accept_workspace_size", "verify_status_string", "verify_abi_version"):
+              "verify_accept_workspace_size", "verify_lmhead_accept",
+              "verify_lmhead_accept_workspace_size", "verify_status_string", "verify_abi_version"):
         assert n in names
 
 
@@ -36,7 +37,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10200
+    assert av.abi_version() == 10300
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
@@ -165,6 +166,36 @@ def test_accept_sampled_argument_validation():
                                      *([None] * 5), 0, None) == 0
     with pytest.raises(ValueError):
         av.verify_accept_sampled(None, None, None, temperature=1.0, seed=-1)
+
+
+def test_lmhead_accept_argument_validation():
+    lib = av.library()
+    n = ctypes.c_size_t(0)
+    assert lib.verify_lmhead_accept_workspace_size(4, 40, 4096, 151936, av.BF16, ctypes.byref(n)) == 0
+    assert n.value >= 40 * 8
+    for args, want in (((4, 40, 4096, 151936, av.F32), av.EUNSUPPORTED),
+                       ((4, 40, 4096, 151936, 7), av.EINVAL),
+                       ((4, 40, 4100, 151936, av.BF16), av.EINVAL),    # hidden not a multiple of 32
+                       ((4, 40, 0, 151936, av.BF16), av.EINVAL),
+                       ((4, 40, 4096, 0, av.BF16), av.EINVAL),
+                       ((4, 40, 4096, 1 << 31, av.BF16), av.EINVAL),
+                       ((-1, 40, 4096, 100, av.BF16), av.EINVAL)):
+        assert lib.verify_lmhead_accept_workspace_size(*args, ctypes.byref(n)) == want, args
+    lib.verify_lmhead_accept_workspace_size(4, 40, 256, 1000, av.BF16, ctypes.byref(n))
+    d = ctypes.c_void_p(0x1000)
+
+    def call(dtype=av.BF16, hid=d, w=d, acc=d, ws=n.value, H=256):
+        return lib.verify_lmhead_accept(4, 40, H, 1000, dtype, hid, w, d, d, None, acc, d, d, d, ws,
+                                        None)
+
+    assert call(dtype=av.F32) == av.EUNSUPPORTED
+    assert call(hid=None) == av.EINVAL
+    assert call(w=None) == av.EINVAL
+    assert call(acc=None) == av.EINVAL
+    assert call(hid=ctypes.c_void_p(0x1008)) == av.EINVAL   # rows are copied in 16-byte pieces
+    assert call(H=250) == av.EINVAL
+    assert call(ws=n.value - 1) == av.EWORKSPACE
+    assert lib.verify_lmhead_accept(0, 0, 256, 1000, av.BF16, *([None] * 8), None, 0, None) == 0
 
 
 def test_budget_argument_validation():

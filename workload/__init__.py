@@ -56,6 +56,7 @@ class Config:
     match: Tuple                    # ("divergence",) | ("prob", p) | ("halves", p_first, p_second)
     windows: Tuple[int, ...] = (0,)  # one attention layer per entry; 0 = full causal
     sinks: bool = False             # per-head attention sink logits in every layer
+    hidden_size: int = 4096         # model width: rows of the LM-head weight
     description: str = ""
 
     def replace(self, **kw) -> "Config":
@@ -71,6 +72,7 @@ CONFIGS = {
     "tiny": Config(
         name="tiny", batch=4, num_q_heads=8, num_kv_heads=2, head_dim=64, dtype="f32",
         vocab=1024, context=("fixed", 256), drafts=("fixed", 4), match=("divergence",),
+        hidden_size=256,
         description="single layer, fp32, drafts planted as argmax up to a random divergence point"),
     "qwen3_8b": Config(
         name="qwen3_8b", batch=32, num_q_heads=32, num_kv_heads=8, head_dim=128, dtype="bf16",
@@ -84,7 +86,7 @@ CONFIGS = {
     "gpt_oss_20b": Config(
         name="gpt_oss_20b", batch=64, num_q_heads=64, num_kv_heads=8, head_dim=64, dtype="bf16",
         vocab=201088, context=("uniform", 4096, 65536), drafts=("fixed", 8), match=("prob", 0.5),
-        windows=(128, 0), sinks=True,
+        windows=(128, 0), sinks=True, hidden_size=2880,
         description="GPT-OSS-20B-shaped verify step: a 128-token sliding-window layer and a full "
                     "layer, both with per-head attention sinks"),
     "long_context": Config(
@@ -250,6 +252,42 @@ def draw_logits(cfg: Config, seed: int, device: str, rows: int, vocab: int,
         xs.scatter_(1, des_t[r0:r1, None], mb[:, None])
         out[r0:r1] = xs
     return out
+
+
+def draw_lmhead(cfg: Config, seed: int, device: str, designated: np.ndarray, *,
+                alpha: float = 8.0, peaked: float = 0.75, vocab: Optional[int] = None,
+                hidden_size: Optional[int] = None):
+    """Final hidden states and an LM-head weight (both bf16) for the fused
+    LM-head path: (hidden [T, H], weight [V, H]).
+
+    weight ~ N(0, 1/H) elementwise, so every row has norm about 1 and the
+    logits <hidden, weight[v]> of an N(0, I) hidden state are about N(0, 1).
+    A fraction `peaked` of the rows (chosen at random) adds alpha * weight[d]
+    for the row's designated token d: its logit gains about alpha and, at
+    alpha = 8, beats the maximum of 10^5 - 10^6 others in nearly every row,
+    so drafts planted as d are mostly accepted, as on a confident model.  The
+    other rows are flat.  No logit is computed here.
+    """
+    import torch
+    V = cfg.vocab if vocab is None else int(vocab)
+    H = cfg.hidden_size if hidden_size is None else int(hidden_size)
+    T = int(designated.shape[0])
+    g = _torch_gen(device, seed, "lmhead")
+    w = torch.empty((V, H), dtype=torch.bfloat16, device=device)
+    scale = 1.0 / math.sqrt(H)
+    step = max(1, (1 << 26) // H)
+    for v0 in range(0, V, step):
+        v1 = min(V, v0 + step)
+        w[v0:v1] = (torch.randn((v1 - v0, H), generator=g, device=device,
+                                dtype=torch.float32) * scale).to(torch.bfloat16)
+    hs = torch.randn((T, H), generator=g, device=device, dtype=torch.float32)
+    rng = np.random.default_rng(_stream_seed(seed, "lmhead-peaked"))
+    pk = rng.random(T) < peaked
+    if T and pk.any():
+        rows = torch.as_tensor(np.nonzero(pk)[0], dtype=torch.int64, device=device)
+        des = torch.as_tensor(designated.astype(np.int64)[pk], device=device)
+        hs[rows] += alpha * w[des].to(torch.float32)
+    return hs.to(torch.bfloat16), w
 
 
 def make_batch(cfg: Config, seed: int, device: str = "cpu", *,
