@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E datasheet peak
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 CALIB_BYTES = 256 << 20  # the plain elementwise kernel of --copy-calibration reads and writes this
 # sources whose change invalidates a stored traffic measurement of the attention call
 KERNEL_SOURCES = ("paper_2608_24004_amd/csrc/verify_attention.hip",
@@ -214,6 +215,39 @@ def accept_timing(av, bt, steps: int, aws):
         us = graph_time_us(fn, steps)
         res[name] = {"us": us, "GBps": nbytes / (us * 1e-6) / 1e9,
                      "logits_per_ns": T * V / (us * 1e3)}
+    return res
+
+
+def lmhead_timing(av, workload, bt, steps: int):
+    """Device time of the LM head fused with greedy acceptance
+    (verify_lmhead_accept) for the step's scored rows: hidden [T, H] and the
+    model's LM-head weight [V, H] in bf16.  Its roofline is the larger of the
+    weight stream over HBM (every weight byte is read once per call while the
+    rows fit one row chunk) and the dense bf16 MFMA work 2 T H V."""
+    import torch
+    cfg = bt.cfg
+    dev = bt.logits.device
+    hidden, weight = workload.draw_lmhead(cfg, 0, str(dev), bt.designated)
+    T, H = hidden.shape
+    V = weight.shape[0]
+    B = len(bt.q_start) - 1
+    outs = [torch.empty(n, dtype=torch.int32, device=dev) for n in (B, B, T, T)]
+    ws = torch.empty(max(1, av.lmhead_accept_workspace_size(B, T, H, V)), dtype=torch.uint8,
+                     device=dev)
+    fn = lambda: av.verify_lmhead_accept(hidden, weight, bt.t_tokens, bt.t_q_start,
+                                         accept_len=outs[0], num_emitted=outs[1], emitted=outs[2],
+                                         argmax_out=outs[3], workspace=ws)
+    fn()
+    us = graph_time_us(fn, steps)
+    nbytes = float(V * H * 2 + T * H * 2)
+    flops = 2.0 * T * H * V
+    t_hbm, t_mfma = nbytes / (HBM_PEAK_GBS * 1e3), flops / (MFMA_BF16_PEAK_TFLOPS * 1e6)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    res = {"us": us, "rows": T, "hidden": H, "vocab": V, "bytes": nbytes, "flops": flops,
+           "GBps": nbytes / (us * 1e-6) / 1e9, "TFLOPs": flops / (us * 1e-6) / 1e12,
+           "bound": bound, "roofline_us": max(t_hbm, t_mfma),
+           "frac": max(t_hbm, t_mfma) / us}
+    del hidden, weight, ws
     return res
 
 
@@ -445,6 +479,8 @@ def main():
     log("KV append (verify_kv_append):", append)
     accept_t = accept_timing(av, bt, K, aws)
     log("acceptance calls:", accept_t)
+    lmhead = lmhead_timing(av, workload, bt, K) if cfg.dtype == "bf16" else None
+    log("LM head fused with acceptance (verify_lmhead_accept):", lmhead)
 
     traffic = stored_traffic(cfg.name)
     if traffic is not None:
@@ -487,6 +523,7 @@ def main():
         "budget_alloc": budget,
         "kv_append": append,
         "accept": accept_t,
+        "lmhead_accept": lmhead,
     }
     print(json.dumps(res), flush=True)
 

@@ -66,10 +66,12 @@ struct LArgs {
 };
 
 // A stage holds 2 * MT * 32 scored rows, then 256 weight rows, each 32 bf16 = four
-// 16-byte chunks.  Chunk c of row r is stored at position c ^ ((r >> 1) & 3)
-// of its row, so that the 8 lanes served together by one ds_read_b128 (rows
-// r .. r + 7 at the same logical chunk) hit distinct banks.
-__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 3); }
+// 16-byte chunks.  Chunk c of row r is stored at position c ^ f(r), f(r) =
+// ((r >> 1) ^ (r >> 3)) & 3: the lanes that one ds_read_b128 phase serves
+// (rows r .. r + 7 or r .. r + 15 at the same logical chunk) then read
+// distinct 16-byte bank groups, whether a phase is 8 lanes over 32 banks or
+// 16 lanes over 64.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ (((r >> 1) ^ (r >> 3)) & 3); }
 
 // Vocabulary quarter q [lo, hi) of workgroup w.
 __device__ __forceinline__ void wave_range(const LArgs& a, int w, int q, int& lo, int& hi) {
@@ -197,6 +199,8 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
         nidx[n] = kLmNone;
     }
 
+    // row tiles of this wavefront's half that hold rows of the current chunk
+    int mtv = MT;
     // one hidden step of a pass: NT = weight tiles of this wavefront (1 or 2)
     auto compute = [&](int st, auto& acc) {
         constexpr int NT = sizeof(acc) / sizeof(acc[0]);
@@ -214,6 +218,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
                                       ws + (wq * kLmWaveRows + t * 32 + c32) * kLmRowBytes + cs));
 #pragma unroll
                 for (int n = 0; n < MT; ++n) {
+                    if (n >= mtv) break;  // row tiles past the chunk
                     const bf16x8_t hf = __builtin_bit_cast(
                         bf16x8_t, *reinterpret_cast<const uint4*>(
                                       hs + ((wg * MT + n) * 32 + c32) * kLmRowBytes + cs));
@@ -316,6 +321,11 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
         }
     };
     for (int mc = 0; mc < a.nchunks; ++mc) {
+        {
+            const int r0 = mc * a.chunk_rows;
+            const int left = min(a.T, r0 + a.chunk_rows) - r0 - wg * MT * 32;
+            mtv = __builtin_amdgcn_readfirstlane(min(MT, max(0, (left + 31) / 32)));
+        }
         for (int p = 0; p < a.passes; ++p) {
             const int nt = min(2, max(0, wtiles - 2 * p));
             if (nt == 2) pass(p, std::integral_constant<int, 2>{});
