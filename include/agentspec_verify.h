@@ -243,9 +243,7 @@ int verify_accept_sampled(int32_t num_seqs, int32_t total_q, int64_t vocab, int6
  *   weight      [vocab][hidden_size] bf16: the LM-head (output embedding)
  *               weight, row v = token v
  *   hidden_size multiple of 32; vocab >= 1 and < 2^31; both pointers 16-byte
- *               aligned (VERIFY_EINVAL otherwise); each matrix below 4 GiB
- *               (2 * vocab * hidden_size and 2 * total_q * hidden_size bytes;
- *               VERIFY_EUNSUPPORTED otherwise)
+ *               aligned (VERIFY_EINVAL otherwise)
  *   dtype       VERIFY_BF16 (VERIFY_F32 returns VERIFY_EUNSUPPORTED)
  * tokens, q_start, argmax_out, accept_len, num_emitted and emitted are
  * verify_accept's.  workspace: at least
