@@ -8,8 +8,8 @@ synthetic inputs already resident in HBM.  Prints one JSON line:
 
   value         verified tokens/s = sum_i (accept_len_i + 1) / step time
   roofline      the attention call: algorithmic bytes per launch / mean launch
-                time (HIP events on the launch stream around each call, in a
-                loop of their own after the timed steps) vs 8 TB/s HBM
+                time (K calls back to back on the launch stream between two HIP
+                events, after the timed steps) vs 8 TB/s HBM
   cpu_baseline  the CPU oracle on a bounded sample of the same step (first
                 requests of the batch, all their heads and logits rows)
 """
@@ -434,18 +434,19 @@ def main():
     wall = time.perf_counter() - wall0
     ms_step = t0.elapsed_time(t1) / K
 
-    # per-launch time of each attention call (roofline): events on the launch
-    # stream around each call, K calls per layer, after the timed region
+    # average duration of one attention call (roofline): K calls of the layer
+    # launched back to back on the launch stream, HIP events at the two ends of
+    # that region, after the timed steps
     attn_ms = []
     for li in range(len(bt.layers)):
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(K)]
-        for e0, e1 in evs:
-            e0.record(stream)
-            attention(li)
-            e1.record(stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        attn_ms.append(float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs])))
+        e0.record(stream)
+        for _ in range(K):
+            attention(li)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        attn_ms.append(e0.elapsed_time(e1) / K)
 
     emitted = int(ne.sum().item())
     proposed = int(bt.num_drafts.sum())

@@ -323,13 +323,23 @@ struct MPtrs {
     const int32_t* q_start;
     uint16_t* out;
     int32_t* unit_start;  // [num_seqs + 1] first unit of each request (schedule pass)
-    float* slot_o;        // [slots][rows_per_group][D] normalised partial outputs
+    float* slot_o;        // [slots][rows_per_group][D] normalised partial outputs (slot_o_index)
     float* slot_lse;      // [slots][rows_per_group]    their log2-sum-exp
 };
 
 struct ReqGeom {
     int q0, n, S, b_lo, nb, rg;
 };
+
+// Offset in slot_o of row lr (within the row group), dims d .. d+3 (d % 4 ==
+// 0), of slot `slot`.  Each 16-row tile of a slot is stored in the order the
+// MFMA output registers hold it: 16-dim column block dt, then lane
+// 16 (d / 4 % 4) + lr % 16, then the four dims.
+template <int D>
+__device__ __forceinline__ int64_t slot_o_index(int64_t slot, int rows_per_group, int lr, int d) {
+    const int lane = ((d >> 2) & 3) * 16 + (lr & 15);
+    return (slot * rows_per_group + (lr & ~15)) * D + ((d >> 4) * kWave + lane) * 4;
+}
 
 __device__ __forceinline__ ReqGeom req_geom(const PArgs& a, const int32_t* __restrict__ q_start,
                                             const int32_t* __restrict__ seq_lens, int i) {
@@ -702,11 +712,14 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
                     *reinterpret_cast<uint2*>(out + hrow * D + d0) = v;
                 }
             } else {
+                // the tile's 16 rows x D floats in register order (see
+                // slot_o_index): each store writes 1 KiB contiguous
                 const float inv = L > 0.f ? 1.f / L : 0.f;
                 const int64_t srow = slot * ROWS + lr;
+                float* tb = slot_o + (slot * ROWS + (wv * TPW + t) * 16) * D + lane * 4;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt)
-                    *reinterpret_cast<f32x4_t*>(slot_o + srow * D + dt * 16 + 4 * lg) = o[t][dt] * inv;
+                    *reinterpret_cast<f32x4_t*>(tb + dt * (kWave * 4)) = o[t][dt] * inv;
                 if (lg == 0) slot_lse[srow] = L > 0.f ? m_r[t] + log2f(L) : -INFINITY;
             }
         }
@@ -792,10 +805,12 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
 
 // Merges the partial slots of pairs cut by workgroup range boundaries, and
 // writes the zero output of rows whose request has no key.  Grid (pairs, row
-// chunks); a thread owns one row and four consecutive output dimensions, so
-// all of a thread's slot reads are independent and issued together.
+// chunks); a thread owns one row and four consecutive output dimensions.  The
+// slots of a row are read kCombineSlots at a time, every load of a round
+// issued before any is used (a pair is cut into a handful of slots, so one
+// round usually covers it), and merged with a running maximum.
 constexpr int kCombineThreads = 256;
-constexpr int kCombineBatch = 4;
+constexpr int kCombineSlots = 8;
 
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
@@ -828,37 +843,40 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
     const int d0 = (threadIdx.x % QUADS) * 4;
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     if (!empty) {
-        // Slots are read in batches of kCombineBatch with every load of a
-        // batch issued before any is used; a slot past the pair's last
-        // workgroup reads as empty (log-sum-exp -inf).
+        // slots of the pair: one per workgroup wf .. wl; a slot holding
+        // log-sum-exp -inf (no visible key in its range) adds nothing
         const int64_t slot0 = (int64_t)P + wf;
         const int ns = wl - wf + 1;
-        float M = -INFINITY;
-        for (int s0 = 0; s0 < ns; s0 += kCombineBatch) {
+        float M = -INFINITY, L = 0.f;
+        for (int s0 = 0; s0 < ns; s0 += kCombineSlots) {
+            float lse[kCombineSlots];
+            f32x4_t o[kCombineSlots];
 #pragma unroll
-            for (int k = 0; k < kCombineBatch; ++k)
-                if (s0 + k < ns) M = fmaxf(M, slot_lse[(slot0 + s0 + k) * ROWS + lr]);
+            for (int k = 0; k < kCombineSlots; ++k) {
+                const int64_t srow = (slot0 + s0 + k) * ROWS + lr;
+                const bool in = s0 + k < ns;
+                lse[k] = in ? slot_lse[srow] : -INFINITY;
+                o[k] = in ? *reinterpret_cast<const f32x4_t*>(
+                                slot_o + slot_o_index<D>(slot0 + s0 + k, ROWS, lr, d0))
+                          : f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+            float m = M;
+#pragma unroll
+            for (int k = 0; k < kCombineSlots; ++k) m = fmaxf(m, lse[k]);
+            if (m == -INFINITY) continue;
+            // rescale what earlier rounds summed (nothing yet: M = -inf gives 0)
+            const float r = __builtin_amdgcn_exp2f(M - m);
+            L *= r;
+            acc *= r;
+#pragma unroll
+            for (int k = 0; k < kCombineSlots; ++k) {
+                const float f = lse[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(lse[k] - m);
+                L += f;
+                acc += f * o[k];
+            }
+            M = m;
         }
         if (M != -INFINITY) {
-            float L = 0.f;
-            for (int s0 = 0; s0 < ns; s0 += kCombineBatch) {
-                float lse[kCombineBatch];
-                f32x4_t o[kCombineBatch];
-#pragma unroll
-                for (int k = 0; k < kCombineBatch; ++k) {
-                    const int64_t srow = (slot0 + s0 + k) * ROWS + lr;
-                    const bool in = s0 + k < ns;
-                    lse[k] = in ? slot_lse[srow] : -INFINITY;
-                    o[k] = in ? *reinterpret_cast<const f32x4_t*>(slot_o + srow * D + d0)
-                              : f32x4_t{0.f, 0.f, 0.f, 0.f};
-                }
-#pragma unroll
-                for (int k = 0; k < kCombineBatch; ++k) {
-                    const float f = lse[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(lse[k] - M);
-                    L += f;
-                    acc += f * o[k];
-                }
-            }
             L += sink_term(a.sinks, g * a.group + rr % a.group, M);
             acc *= 1.f / L;
         }
@@ -1138,7 +1156,7 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
 // Schedule pass, then the persistent kernel of the plan's shape, then the
 // merge of partial slots.  Returns false if the plan names no known shape.
 bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, int head_dim,
-                    hipStream_t stream) {
+                    int max_rows, hipStream_t stream) {
     if (!a.inline_sched)
         hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
                            m.unit_start);
@@ -1149,7 +1167,9 @@ bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, int head
                            m.slot_o, m.slot_lse);
         const int64_t pairs = (int64_t)a.num_seqs * a.hkv * a.rg_max;
         constexpr int RPB = kCombineThreads / (S::D / 4);
-        const unsigned chunks = (unsigned)((a.rows_per_group + RPB - 1) / RPB);
+        // rows of a row group: at most rows_per_group, at most G * max_q_len
+        const int group_rows = std::max(1, std::min(a.rows_per_group, max_rows));
+        const unsigned chunks = (unsigned)((group_rows + RPB - 1) / RPB);
         if (pairs > 0)
             hipLaunchKernelGGL((attn_combine_slots<S::D>), dim3((unsigned)pairs, chunks),
                                dim3(kCombineThreads), 0, stream, a, m.seq_lens, m.q_start,
@@ -1237,7 +1257,9 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         a.spb = pl.spb;
         a.inline_sched = p.num_seqs <= kInlineSchedSeqs;
         a.sinks = sinks;
-        if (!launch_persist(a, m, pl, p.head_dim, stream)) return VERIFY_EUNSUPPORTED;
+        const int64_t max_rows = (int64_t)a.group * std::max(1, max_q_len);
+        if (!launch_persist(a, m, pl, p.head_dim, (int)std::min<int64_t>(max_rows, 1 << 30), stream))
+            return VERIFY_EUNSUPPORTED;
         return check_launch();
     }
 
