@@ -391,6 +391,10 @@ __global__ __launch_bounds__(kArgmaxThreads) void sample_chunks(
     }
 }
 
+// Partials a lane of accept_scan reduces at most: rows with more chunks
+// (the fused LM head leaves one per workgroup) share a row among lanes.
+constexpr int kScanChunksPerLane = 16;
+
 __global__ __launch_bounds__(kWave) void accept_scan(
     int num_seqs, const int32_t* __restrict__ q_start, const int32_t* __restrict__ tokens,
     const uint64_t* __restrict__ partial, int nchunks, int32_t* __restrict__ argmax_out,
@@ -408,25 +412,34 @@ __global__ __launch_bounds__(kWave) void accept_scan(
     const int k = n - 1;   // drafts; draft j+1 sits at tokens[q0 + j + 1]
     int m = -1;            // accepted drafts, once known
     int32_t bonus = 0;
-    for (int j0 = 0; j0 < n; j0 += kWave) {
-        // each lane reduces the chunk partials of one row to its argmax
-        const int j = j0 + lane;
-        int32_t am = 0;
+    // L lanes share a row (a power of two; each lane reads at most
+    // kScanChunksPerLane of the row's partials), R = 64 / L rows per round
+    int L = 1;
+    while (L < kWave && L * kScanChunksPerLane < nchunks) L <<= 1;
+    const int R = kWave / L;
+    const int sub = lane & (L - 1);
+    for (int j0 = 0; j0 < n; j0 += R) {
+        const int j = j0 + lane / L;
+        uint64_t best = 0;
         if (j < n) {
             const uint64_t* pr = partial + (int64_t)(q0 + j) * nchunks;
-            uint64_t best = 0;
-            for (int c = 0; c < nchunks; ++c) best = pr[c] > best ? pr[c] : best;
-            am = (int32_t)(0xffffffffu - (uint32_t)best);
-            argmax_out[q0 + j] = am;
+            for (int c = sub; c < nchunks; c += L) best = pr[c] > best ? pr[c] : best;
         }
+        for (int o = 1; o < L; o <<= 1) {  // within the row's aligned group of L lanes
+            const uint64_t other = shfl_xor_u64(best, o);
+            best = other > best ? other : best;
+        }
+        const int32_t am = (int32_t)(0xffffffffu - (uint32_t)best);
+        const bool lead = sub == 0 && j < n;
+        if (lead) argmax_out[q0 + j] = am;
         if (m < 0) {
             // stop at the first row whose argmax disagrees with the next
             // draft, or at row k, which has no draft after it
-            const bool stop = (j < n) && (j == k || am != tokens[q0 + j + 1]);
+            const bool stop = lead && (j == k || am != tokens[q0 + j + 1]);
             const uint64_t ballot = __ballot(stop);
             if (ballot) {
                 const int first = (int)__builtin_ctzll(ballot);
-                m = j0 + first;
+                m = j0 + first / L;
                 bonus = __shfl(am, first);
             }
         }
