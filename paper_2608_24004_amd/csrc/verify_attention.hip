@@ -1012,10 +1012,12 @@ bool with_shape(int d, int nw, int tpw, F&& f) {
         return true;                                       \
     }
     AVERIFY_SHAPE(128, 1, 1)
+    AVERIFY_SHAPE(128, 1, 3)
     AVERIFY_SHAPE(128, 2, 1)
     AVERIFY_SHAPE(128, 2, 2)
     AVERIFY_SHAPE(128, 4, 2)
     AVERIFY_SHAPE(64, 1, 1)
+    AVERIFY_SHAPE(64, 1, 5)
     AVERIFY_SHAPE(64, 2, 1)
     AVERIFY_SHAPE(64, 4, 1)
     AVERIFY_SHAPE(64, 4, 2)
@@ -1107,9 +1109,11 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
         } else if (p->head_dim == 128) {
             pl.nw = tiles <= 4 ? 2 : 4;
             pl.tpw = tiles == 2 ? 1 : 2;
+            if (tiles == 3 && nb_max >= 64) { pl.nw = 1; pl.tpw = 3; }
         } else {
             pl.nw = tiles <= 2 ? 2 : 4;
             pl.tpw = (int)std::min<int64_t>(4, (tiles + pl.nw - 1) / pl.nw);
+            if (tiles == 5 && nb_max >= 64) { pl.nw = 1; pl.tpw = 5; }
         }
         const int64_t per = (int64_t)pl.nw * pl.tpw * 16;
         pl.rg_max = (int)((rows + per - 1) / per);

@@ -218,6 +218,17 @@ def test_attention_split_invariance_and_degenerate():
         _check_paged(p, split=split, what="split=%d" % split)
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(64, 8, 64), (32, 8, 128), (16, 2, 64)])
+def test_attention_long_pairs(hq, hkv, d):
+    # pairs of 64 blocks and more run on the one-wavefront shapes (72 rows at
+    # D 64, 36 rows at D 128); shorter pairs in the same batch, every row checked
+    say("attn long pairs", hq, hkv, d)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype="bf16",
+                     contexts=[1500, 3100, 40, 1030, 0], drafts=[8, 8, 3, 8, 8], seed=hq + d)
+    for split in (0, 1, 3, 100):
+        _check_paged(p, split=split, what="long pairs split=%d" % split)
+
+
 @pytest.mark.parametrize("name", list(workload.CONFIGS))
 def test_attention_full_size_sampled(name):
     cfg = workload.CONFIGS[name]
