@@ -37,35 +37,96 @@ __device__ __forceinline__ int clamp_len(int len, int max_len) { return min(max(
 // Score of request i (one wavefront): candidate rows r0 .. r0 + n - 1, whose
 // lengths and tokens come from len_of(r) and tok_at(r, k) (LDS or global).
 // Writes score, agree, prefix_len and source of request i from lane 0.
+//
+// The candidates that share a first token form a group; the group's common
+// prefix is the longest prefix all of its members start with, i.e. the
+// minimum over members of each member's common prefix with any one fixed
+// member.  With at most one candidate per lane (n <= 64), every lane compares
+// its candidate with its group's lowest row only, four tokens at a time, and
+// the group sizes and minima are gathered across lanes; larger candidate sets
+// take each candidate against every member of its group in turn.
 template <typename LenF, typename TokF>
 __device__ __forceinline__ void score_request(int i, int r0, int n, LenF len_of, TokF tok_at,
                                               double g_min, int lane, double* score,
                                               int32_t* agree, int32_t* prefix_len,
                                               int32_t* source) {
-    // Per candidate a (lanes stride over them): size c_a of its first-token
-    // group and l_a, the prefix it shares with every member (the group's
-    // longest common prefix).
+    // Per candidate a: size c of its first-token group and l, the group's
+    // common prefix; then the wavefront's choice below.
     int best_c = 0, best_l = 0, best_tok = INT32_MAX;
-    for (int a = lane; a < n; a += kWave) {
-        const int ra = r0 + a;
-        const int la = len_of(ra);
-        if (la == 0) continue;
-        const int t0 = tok_at(ra, 0);
-        int c = 0, l = la;
+    if (n <= kWave) {
+        const int a = lane;
+        const bool in = a < n;
+        const int la = in ? len_of(r0 + a) : 0;
+        const bool valid = la > 0;
+        const int t0 = valid ? tok_at(r0 + a, 0) : 0;
+        // group size and lowest member (rows ascend with the lane)
+        int c = 0, rep = a;
         for (int b = 0; b < n; ++b) {
-            const int rb = r0 + b;
-            const int lb = len_of(rb);
-            if (lb == 0 || tok_at(rb, 0) != t0) continue;
-            ++c;
-            const int m = min(l, lb);
-            int k = 1;
-            while (k < m && tok_at(ra, k) == tok_at(rb, k)) ++k;
-            l = min(l, k);
+            const int vb = __builtin_amdgcn_readlane((int)valid, b);
+            const int tb = __builtin_amdgcn_readlane(t0, b);
+            if (valid && vb && tb == t0) {
+                ++c;
+                rep = min(rep, b);
+            }
         }
-        if (c > best_c || (c == best_c && (l > best_l || (l == best_l && t0 < best_tok)))) {
+        // common prefix with the lowest member (at least the first token)
+        const int lrep = __shfl(la, rep);
+        const int m = min(la, lrep);
+        int k = 1;
+        if (valid) {
+            const int ra = r0 + a, rr = r0 + rep;
+            bool same = true;
+            while (same && k < m) {
+                int x[4], y[4];
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    const int kk = min(k + d, m - 1);
+                    x[d] = tok_at(ra, kk);
+                    y[d] = tok_at(rr, kk);
+                }
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    if (same && k < m && x[d] == y[d]) ++k;
+                    else same = false;
+                }
+            }
+        }
+        const int lcp = valid ? k : 0;
+        // the group's common prefix: the minimum over its members
+        int l = la;
+        for (int b = 0; b < n; ++b) {
+            const int vb = __builtin_amdgcn_readlane((int)valid, b);
+            const int tb = __builtin_amdgcn_readlane(t0, b);
+            const int lb = __builtin_amdgcn_readlane(lcp, b);
+            if (valid && vb && tb == t0) l = min(l, lb);
+        }
+        if (valid) {
             best_c = c;
             best_l = l;
             best_tok = t0;
+        }
+    } else {
+        for (int a = lane; a < n; a += kWave) {
+            const int ra = r0 + a;
+            const int la = len_of(ra);
+            if (la == 0) continue;
+            const int t0 = tok_at(ra, 0);
+            int c = 0, l = la;
+            for (int b = 0; b < n; ++b) {
+                const int rb = r0 + b;
+                const int lb = len_of(rb);
+                if (lb == 0 || tok_at(rb, 0) != t0) continue;
+                ++c;
+                const int m = min(l, lb);
+                int k = 1;
+                while (k < m && tok_at(ra, k) == tok_at(rb, k)) ++k;
+                l = min(l, k);
+            }
+            if (c > best_c || (c == best_c && (l > best_l || (l == best_l && t0 < best_tok)))) {
+                best_c = c;
+                best_l = l;
+                best_tok = t0;
+            }
         }
     }
     // Wavefront choice: largest group, then longest prefix, then smallest token.
@@ -128,16 +189,20 @@ __global__ __launch_bounds__(kWave) void budget_score(
 
 // Draft lengths, q_start, tokens and seq_lens of the batch (one workgroup of
 // kAssignThreads; every thread calls it).  G = sum_i g_i in ascending i fixes
-// the rounding of every share.
+// the rounding of every share.  Candidate tokens come from tok_at(row, k)
+// (LDS or global); the drafts of each round of requests are copied by the
+// whole workgroup, one (request, position) per thread.
+template <typename TokF>
 __device__ __forceinline__ void assign_batch(
-    int num_seqs, int max_len, const int32_t* __restrict__ cand_len,
-    const int32_t* __restrict__ cand_tokens, const int32_t* __restrict__ last_token,
+    int num_seqs, int max_len, const int32_t* __restrict__ cand_len, TokF tok_at,
+    const int32_t* __restrict__ last_token,
     const int32_t* __restrict__ ctx_len, double alpha, const double* score,
     const int32_t* prefix_len, const int32_t* source, int32_t* __restrict__ draft_len,
     int32_t* __restrict__ q_start, int32_t* __restrict__ tokens, int32_t* __restrict__ seq_lens) {
     __shared__ double G_s;
     __shared__ int wsum[kAssignThreads / kWave];
     __shared__ int carry_s;
+    __shared__ int r_q0[kAssignThreads], r_len[kAssignThreads], r_src[kAssignThreads];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
     if (wv == 0) {
         // G in ascending i, as one sequential sum: wavefront 0 loads 64 scores
@@ -197,14 +262,21 @@ __device__ __forceinline__ void assign_batch(
         }
         __syncthreads();
         const int q0 = carry_s + (wv > 0 ? wsum[wv - 1] : 0) + x - u;
+        r_q0[tid] = q0;
+        r_len[tid] = L;
+        r_src[tid] = max(src, 0);
         if (i < num_seqs) {
             q_start[i + 1] = q0 + L + 1;
             tokens[q0] = last_token[i];
-            const int32_t* st = cand_tokens + (int64_t)max(src, 0) * max_len;
-            for (int j = 0; j < L; ++j) tokens[q0 + 1 + j] = st[j];
             if (ctx_len) seq_lens[i] = ctx_len[i] + L + 1;
         }
         __syncthreads();
+        // the round's drafts: position j of request base + t
+        const int nr = min(kAssignThreads, num_seqs - base);
+        for (int e = tid; e < nr * max_len; e += kAssignThreads) {
+            const int t = e / max_len, j = e - t * max_len;
+            if (j < r_len[t]) tokens[r_q0[t] + 1 + j] = tok_at(r_src[t], j);
+        }
         if (tid == kAssignThreads - 1) carry_s = q0 + u;
         __syncthreads();
     }
@@ -217,8 +289,9 @@ __global__ __launch_bounds__(kAssignThreads) void budget_assign(
     const int32_t* __restrict__ prefix_len, const int32_t* __restrict__ source,
     int32_t* __restrict__ draft_len, int32_t* __restrict__ q_start, int32_t* __restrict__ tokens,
     int32_t* __restrict__ seq_lens) {
-    assign_batch(num_seqs, max_len, cand_len, cand_tokens, last_token, ctx_len, alpha, score,
-                 prefix_len, source, draft_len, q_start, tokens, seq_lens);
+    assign_batch(num_seqs, max_len, cand_len,
+                 [&](int r, int k) { return cand_tokens[(int64_t)r * max_len + k]; }, last_token,
+                 ctx_len, alpha, score, prefix_len, source, draft_len, q_start, tokens, seq_lens);
 }
 
 // Batches whose candidates fit kFusedLdsBytes of LDS run as one workgroup:
@@ -254,8 +327,9 @@ __global__ __launch_bounds__(kAssignThreads) void budget_fused(
             g_min, lane, score, agree, prefix_len, source);
     }
     __syncthreads();
-    assign_batch(num_seqs, max_len, cand_len, cand_tokens, last_token, ctx_len, alpha, score,
-                 prefix_len, source, draft_len, q_start, tokens, seq_lens);
+    assign_batch(num_seqs, max_len, cand_len, [&](int r, int k) { return s_tok[r * max_len + k]; },
+                 last_token, ctx_len, alpha, score, prefix_len, source, draft_len, q_start, tokens,
+                 seq_lens);
 }
 
 }  // namespace
