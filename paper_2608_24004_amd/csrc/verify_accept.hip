@@ -422,8 +422,19 @@ __global__ __launch_bounds__(kWave) void accept_scan(
         const int j = j0 + lane / L;
         uint64_t best = 0;
         if (j < n) {
+            // all of a lane's loads of a pass are issued before any is
+            // compared, so a pass costs one memory latency, not sixteen
             const uint64_t* pr = partial + (int64_t)(q0 + j) * nchunks;
-            for (int c = sub; c < nchunks; c += L) best = pr[c] > best ? pr[c] : best;
+            for (int c0 = sub; c0 < nchunks; c0 += L * kScanChunksPerLane) {
+                uint64_t v[kScanChunksPerLane];
+#pragma unroll
+                for (int t = 0; t < kScanChunksPerLane; ++t) {
+                    const int c = c0 + t * L;
+                    v[t] = c < nchunks ? pr[c] : 0;
+                }
+#pragma unroll
+                for (int t = 0; t < kScanChunksPerLane; ++t) best = v[t] > best ? v[t] : best;
+            }
         }
         for (int o = 1; o < L; o <<= 1) {  // within the row's aligned group of L lanes
             const uint64_t other = shfl_xor_u64(best, o);
