@@ -67,11 +67,24 @@ struct LArgs {
 
 // A stage holds 2 * MT * 32 scored rows, then 256 weight rows, each 32 bf16 = four
 // 16-byte chunks.  Chunk c of row r is stored at position c ^ f(r), f(r) =
-// ((r >> 1) ^ (r >> 3)) & 3: the lanes that one ds_read_b128 phase serves
-// (rows r .. r + 7 or r .. r + 15 at the same logical chunk) then read
-// distinct 16-byte bank groups, whether a phase is 8 lanes over 32 banks or
-// 16 lanes over 64.
-__device__ __forceinline__ int swz(int r, int c) { return c ^ (((r >> 1) ^ (r >> 3)) & 3); }
+// 2 ((r >> 2) & 1) + ((r >> 3) & 1).  A ds_read_b128 of 32 rows at one logical
+// chunk (two chunks per row, one per half-wave) then takes gfx950's minimum of
+// four LDS cycles; measured with the LDS bank-conflict counter, the unswizzled
+// layout takes sixteen and an XOR of bits 1-3 eight.
+__device__ __forceinline__ int swz(int r, int c) {
+    return c ^ (((r >> 2) & 1) << 1) ^ ((r >> 3) & 1);
+}
+
+// f(std::integral_constant<int, v>) for a runtime v in [0, M].
+template <int M, typename F>
+__device__ __forceinline__ void with_count(int v, F&& f) {
+    if constexpr (M == 0) {
+        f(std::integral_constant<int, 0>{});
+    } else {
+        if (v >= M) f(std::integral_constant<int, M>{});
+        else with_count<M - 1>(v, f);
+    }
+}
 
 // Vocabulary quarter q [lo, hi) of workgroup w.
 __device__ __forceinline__ void wave_range(const LArgs& a, int w, int q, int& lo, int& hi) {
@@ -201,31 +214,36 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
 
     // row tiles of this wavefront's half that hold rows of the current chunk
     int mtv = MT;
-    // one hidden step of a pass: NT = weight tiles of this wavefront (1 or 2)
-    auto compute = [&](int st, auto& acc) {
+    // One hidden step of a pass: NT = weight tiles of this wavefront (1 or 2),
+    // MV = row tiles holding rows of the chunk (a compile-time count, so that
+    // the step is straight-line code: every fragment of a 16-dim half is
+    // read before its products, one LDS round trip per half instead of one
+    // per row tile).
+    auto compute = [&](int st, auto& acc, auto mv) {
         constexpr int NT = sizeof(acc) / sizeof(acc[0]);
-        {
+        constexpr int MV = decltype(mv)::value;
+        if constexpr (MV > 0) {
             const uint8_t* hs = stage[st];
             const uint8_t* ws = stage[st] + HROWS * kLmRowBytes;
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int cs = swz(c32, 2 * j + h) * 16;  // same swizzle for every tile row
-                bf16x8_t wf[NT];
+                bf16x8_t wf[NT], hf[MV];
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
                     wf[t] = __builtin_bit_cast(
                         bf16x8_t, *reinterpret_cast<const uint4*>(
                                       ws + (wq * kLmWaveRows + t * 32 + c32) * kLmRowBytes + cs));
 #pragma unroll
-                for (int n = 0; n < MT; ++n) {
-                    if (n >= mtv) break;  // row tiles past the chunk
-                    const bf16x8_t hf = __builtin_bit_cast(
+                for (int n = 0; n < MV; ++n)
+                    hf[n] = __builtin_bit_cast(
                         bf16x8_t, *reinterpret_cast<const uint4*>(
                                       hs + ((wg * MT + n) * 32 + c32) * kLmRowBytes + cs));
 #pragma unroll
+                for (int n = 0; n < MV; ++n)
+#pragma unroll
                     for (int t = 0; t < NT; ++t)
-                        acc[t][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[t], hf, acc[t][n], 0, 0, 0);
-                }
+                        acc[t][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[t], hf[n], acc[t][n], 0, 0, 0);
             }
         }
     };
@@ -311,12 +329,15 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
             for (int t = 0; t < NT; ++t)
 #pragma unroll
                 for (int n = 0; n < MT; ++n) acc[t][n] = f32x16_t{};
-            int ks = 0;
-            do {  // nk >= 1
-                step();
-                compute(st, acc);
-                st = st == kLmStages - 1 ? 0 : st + 1;
-            } while (++ks < a.nk);
+            auto walk = [&](auto mv) {
+                int ks = 0;
+                do {  // nk >= 1
+                    step();
+                    compute(st, acc, mv);
+                    st = st == kLmStages - 1 ? 0 : st + 1;
+                } while (++ks < a.nk);
+            };
+            with_count<MT>(mtv, walk);
             end_pass(p, acc);
         }
     };
