@@ -12,21 +12,21 @@
 // scored row (column l % 32) and 16 vocabulary entries, so most of the argmax
 // is a running compare inside the lane.
 //
-// Work split.  lmhead_argmax launches one 8-wavefront workgroup per compute
-// unit (two wavefronts per SIMD).  Workgroup w owns the vocabulary range
+// Work split.  lmhead_argmax launches one 12-wavefront workgroup per compute
+// unit (three wavefronts per SIMD).  Workgroup w owns the vocabulary range
 // [V w / N, V (w+1) / N); wavefront (q, g) takes vocabulary quarter q of it and
-// scored-row half g of the current row chunk, and walks its quarter in passes
-// of two 32-entry tiles (the last pass may hold one).  Per pass, the hidden
-// dimension is walked in steps of 32: each step's weight rows (256 = 4
-// quarters x 64) and scored rows (up to 320 = 2 halves x 5 tiles of 32) are
-// copied once, 16 bytes per lane, from global memory into a ring of four LDS
-// stages (three steps in flight), read from there as MFMA operands by every
-// wavefront that needs them, and accumulated in registers (2 x 5 tiles of 16
-// floats per lane).  At the end of a pass the lane folds its logits into a
-// running (maximum, first index, first NaN) per scored row.  Every weight
-// byte is read from HBM once per row chunk; the hidden states (a few MB) come
-// from L2.  More than 320 scored rows are cut into row chunks, each walking
-// the weights again.
+// scored-row group g (of three) of the current row chunk, and walks its
+// quarter in passes of two 32-entry tiles (the last pass may hold one).  Per
+// pass, the hidden dimension is walked in steps of 32: each step's weight rows
+// (256 = 4 quarters x 64) and scored rows (up to 288 = 3 groups x 3 tiles of
+// 32) are copied once, 16 bytes per lane, from global memory into a ring of
+// four LDS stages (three steps in flight), read from there as MFMA operands by
+// every wavefront that needs them, and accumulated in registers (2 x 3 tiles
+// of 16 floats per lane).  At the end of a pass the lane folds its logits
+// into a running (maximum, first index, first NaN) per scored row.  Every
+// weight byte is read from HBM once per row chunk; the hidden states (a few
+// MB) come from L2.  More than 288 scored rows are cut into row chunks, each
+// walking the weights again.
 //
 // After the last pass the wavefronts' maxima are merged into one packed
 // (order key, ~index) word per (scored row, workgroup), the format of
@@ -42,7 +42,8 @@ namespace {
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
-constexpr int kLmWaves = 8;                        // 4 vocabulary quarters x 2 row halves
+constexpr int kLmRowGroups = 3;                    // scored-row groups per workgroup
+constexpr int kLmWaves = 4 * kLmRowGroups;         // 4 vocabulary quarters x the row groups
 constexpr int kLmQuarters = 4;
 constexpr int kLmThreads = kLmWaves * kWave;
 constexpr int kLmStep = 32;                        // hidden dims per LDS stage
@@ -50,7 +51,7 @@ constexpr int kLmStages = 4;                       // LDS ring stages
 constexpr int kLmDepth = kLmStages - 1;            // stages in flight
 constexpr int kLmWaveRows = 64;                    // weight rows per wavefront and pass
 constexpr int kLmWRows = kLmQuarters * kLmWaveRows;  // weight rows per stage (256)
-constexpr int kLmMaxTiles = 5;                     // scored-row tiles of 32 per wavefront
+constexpr int kLmMaxTiles = 3;                     // scored-row tiles of 32 per wavefront
 constexpr int kLmRowBytes = kLmStep * 2;           // one row of a stage: 32 bf16 = 64 bytes
 constexpr uint32_t kLmNone = 0xffffffffu;
 
@@ -59,13 +60,13 @@ struct LArgs {
     int H;           // hidden size (multiple of kLmStep)
     int V;           // vocabulary
     int nwg;         // workgroups (vocabulary ranges)
-    int chunk_rows;  // scored rows per row chunk (<= 64 * MT)
+    int chunk_rows;  // scored rows per row chunk (<= kLmRowGroups * 32 * MT)
     int nchunks;     // row chunks
     int passes;      // passes of two tiles per wavefront over its vocabulary quarter
     int nk;          // hidden steps per pass (H / kLmStep)
 };
 
-// A stage holds 2 * MT * 32 scored rows, then 256 weight rows, each 32 bf16 = four
+// A stage holds kLmRowGroups * MT * 32 scored rows, then 256 weight rows, each 32 bf16 = four
 // 16-byte chunks.  Chunk c of row r is stored at position c ^ f(r), f(r) =
 // 2 ((r >> 2) & 1) + ((r >> 3) & 1).  A ds_read_b128 of 32 rows at one logical
 // chunk (two chunks per row, one per half-wave) then takes gfx950's minimum of
@@ -107,10 +108,11 @@ __device__ __forceinline__ void fold(float x, uint32_t v, bool ok, float& best, 
 }
 
 template <int MT>
-__global__ __launch_bounds__(kLmThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(kLmThreads)
+__attribute__((amdgpu_waves_per_eu(kLmRowGroups, kLmRowGroups)))
 void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __restrict__ wt,
                    uint64_t* __restrict__ partial) {
-    constexpr int HROWS = 2 * MT * 32;                   // scored rows per stage
+    constexpr int HROWS = kLmRowGroups * MT * 32;        // scored rows per stage
     constexpr int STAGE = (HROWS + kLmWRows) * kLmRowBytes;
     constexpr int NI = (HROWS + kLmWRows) * 4 / kWave;   // 1 KiB global->LDS loads per stage
     constexpr int CPT_HI = (NI + kLmWaves - 1) / kLmWaves;
@@ -128,7 +130,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     const int c32 = lane & 31, h = lane >> 5;
     const int cpt = wv < NI % kLmWaves || NI % kLmWaves == 0 ? CPT_HI : CPT_LO;
     const int wq = wv % kLmQuarters;  // vocabulary quarter
-    const int wg = wv / kLmQuarters;  // scored-row half: rows [32 MT wg, 32 MT (wg + 1)) of a chunk
+    const int wg = wv / kLmQuarters;  // row group: rows [32 MT wg, 32 MT (wg + 1)) of a chunk
 
     // this wavefront's vocabulary quarter and the workgroup's range
     int vlo, vhi;
@@ -142,7 +144,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     const int units = a.nchunks * a.passes * a.nk;
 
     // ---- loader: unit u = (row chunk, pass, hidden step); one unit fills one
-    // stage.  Load c2 of this wavefront is stage load i = 8 c2 + wv, covering
+    // stage.  Load c2 of this wavefront is stage load i = 12 c2 + wv, covering
     // stage chunks [64 i, 64 i + 64); lane l moves chunk 64 i + l.
     const uint16_t* src[CPT_HI];
     int l_u = 0, l_ks = 0;
@@ -212,7 +214,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
         nidx[n] = kLmNone;
     }
 
-    // row tiles of this wavefront's half that hold rows of the current chunk
+    // row tiles of this wavefront's group that hold rows of the current chunk
     int mtv = MT;
     // One hidden step of a pass: NT = weight tiles of this wavefront (1 or 2),
     // MV = row tiles holding rows of the chunk (a compile-time count, so that
@@ -394,10 +396,10 @@ LmPlan plan_lmhead(int32_t total_q, int32_t hidden_size, int64_t vocab) {
     a.H = hidden_size;
     a.V = (int)vocab;
     a.nwg = (int)std::min<int64_t>(lm_cus(), vocab);
-    constexpr int max_rows = 2 * kLmMaxTiles * 32;
+    constexpr int max_rows = kLmRowGroups * kLmMaxTiles * 32;
     a.nchunks = std::max(1, (total_q + max_rows - 1) / max_rows);
     a.chunk_rows = std::max(1, (total_q + a.nchunks - 1) / a.nchunks);
-    pl.mt = (a.chunk_rows + 63) / 64;
+    pl.mt = (a.chunk_rows + kLmRowGroups * 32 - 1) / (kLmRowGroups * 32);
     const int64_t wg_len = (vocab + a.nwg - 1) / a.nwg;
     const int64_t q_len = (wg_len + kLmQuarters - 1) / kLmQuarters;
     const int64_t tiles = (q_len + 31) / 32;
@@ -450,8 +452,6 @@ extern "C" int verify_lmhead_accept(int32_t num_seqs, int32_t total_q, int32_t h
             case 1: launch_lmhead<1>(pl.a, hs, ws, partial, stream); break;
             case 2: launch_lmhead<2>(pl.a, hs, ws, partial, stream); break;
             case 3: launch_lmhead<3>(pl.a, hs, ws, partial, stream); break;
-            case 4: launch_lmhead<4>(pl.a, hs, ws, partial, stream); break;
-            case 5: launch_lmhead<5>(pl.a, hs, ws, partial, stream); break;
             default: return VERIFY_EUNSUPPORTED;
         }
         if (check_launch() != VERIFY_OK) return VERIFY_EHIP;

@@ -93,6 +93,8 @@ CASES = [
     ([9] * 4, 256, 1024),
     ([17, 0, 33, 15], 128, 5003),
     ([65], 96, 777),
+    ([9] * 32, 256, 3001),               # 288 rows: one full row chunk
+    ([9] * 32 + [1], 128, 3001),         # 289 rows: a second chunk of one row
     ([9] * 36, 256, 3001),               # 324 rows: two row chunks
     ([33] * 21, 64, 2048),               # 693 rows: three row chunks
     ([3, 8, 1], 2880, 4099),
