@@ -132,6 +132,52 @@ def _dev_ptr(t, name, dtype=None):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _expect(t, name, shape=None, dtype=None, device=None):
+    """Check a caller tensor before its pointer crosses the ABI.
+
+    The kernels index device memory by the sizes passed beside the pointers,
+    so a tensor smaller than those sizes would be read or written out of
+    bounds, and one on another device would be read through the wrong
+    address space."""
+    if t is None:
+        raise ValueError("%s is required" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, the call runs on %s" % (name, t.device, device))
+
+
+def _check_attention_tensors(q, k_cache, v_cache, block_tables, seq_lens=None, q_start=None,
+                             sinks=None, out=None, workspace=None):
+    import torch
+    if q.dim() != 3:
+        raise ValueError("q must be [T, Hq, D], got %s" % (tuple(q.shape),))
+    T, Hq, D = q.shape
+    if k_cache.dim() != 5:
+        raise ValueError("k_cache must be [num_blocks, Hkv, D/x, 16, x], got %s" % (tuple(k_cache.shape),))
+    nb, hkv = k_cache.shape[0], k_cache.shape[1]
+    x = 16 // q.element_size()
+    dev, i32 = q.device, torch.int32
+    _expect(k_cache, "k_cache", (nb, hkv, D // x, 16, x), q.dtype, dev)
+    _expect(v_cache, "v_cache", (nb, hkv, D, 16), q.dtype, dev)
+    if block_tables.dim() != 2:
+        raise ValueError("block_tables must be [B, max_blocks], got %s" % (tuple(block_tables.shape),))
+    B = block_tables.shape[0]
+    _expect(block_tables, "block_tables", None, i32, dev)
+    if seq_lens is not None:
+        _expect(seq_lens, "seq_lens", (B,), i32, dev)
+    if q_start is not None:
+        _expect(q_start, "q_start", (B + 1,), i32, dev)
+    if sinks is not None:
+        _expect(sinks, "sinks", (Hq,), torch.float32, dev)
+    if out is not None:
+        _expect(out, "out", tuple(q.shape), q.dtype, dev)
+    if workspace is not None:
+        _expect(workspace, "workspace", None, None, dev)
+
+
 def _stream_ptr(stream, device):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream(device)
@@ -179,6 +225,8 @@ def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, ma
     float32 device tensor of per-head sink logits.  Returns `out`.
     """
     import torch
+    _check_attention_tensors(q, k_cache, v_cache, block_tables, seq_lens, q_start, sinks, out,
+                             workspace)
     params = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
     if out is None:
         out = torch.empty_like(q)
@@ -210,10 +258,21 @@ def accept_workspace_size(num_seqs: int, total_q: int, vocab: int, dtype_code: i
 
 def _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace):
     import torch
+    if logits.dim() != 2:
+        raise ValueError("logits must be [T, V], got %s" % (tuple(logits.shape),))
     T, V = logits.shape
+    if q_start.dim() != 1 or q_start.shape[0] < 1:
+        raise ValueError("q_start must be [B + 1], got %s" % (tuple(q_start.shape),))
     B = q_start.shape[0] - 1
     dev = logits.device
     i32 = torch.int32
+    _expect(q_start, "q_start", None, i32, dev)
+    for name, t, n in (("argmax_out", argmax_out, T), ("accept_len", accept_len, B),
+                       ("num_emitted", num_emitted, B), ("emitted", emitted, T)):
+        if t is not None:
+            _expect(t, name, (n,), i32, dev)
+    if workspace is not None:
+        _expect(workspace, "workspace", None, None, dev)
     code = _dtype_code(logits)
     if argmax_out is None:
         argmax_out = torch.empty(T, dtype=i32, device=dev)
@@ -241,6 +300,7 @@ def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, 
     i32 = torch.int32
     B, T, V, code, argmax_out, accept_len, num_emitted, emitted, workspace, ws_have = \
         _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace)
+    _expect(tokens, "tokens", (T,), i32, logits.device)
     rc = library().verify_accept(
         B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
         _dev_ptr(q_start, "q_start", i32), _dev_ptr(argmax_out, "argmax_out", i32),
@@ -268,6 +328,7 @@ def verify_accept_sampled(logits, tokens, q_start, *, temperature: float, seed: 
         raise ValueError("seed must fit 64 bits and offset 32 bits, unsigned")
     B, T, V, code, sampled_out, accept_len, num_emitted, emitted, workspace, ws_have = \
         _accept_buffers(logits, q_start, sampled_out, accept_len, num_emitted, emitted, workspace)
+    _expect(tokens, "tokens", (T,), i32, logits.device)
     rc = library().verify_accept_sampled(
         B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
         _dev_ptr(q_start, "q_start", i32), float(temperature), int(seed), int(offset),
@@ -299,12 +360,25 @@ def verify_lmhead_accept(hidden, weight, tokens, q_start, *, argmax_out=None, ac
     """
     import torch
     i32 = torch.int32
+    if hidden.dim() != 2 or weight.dim() != 2:
+        raise ValueError("hidden must be [T, H] and weight [V, H]")
     T, H = hidden.shape
     V, H2 = weight.shape
     if H != H2:
         raise ValueError("hidden sizes differ: %d vs %d" % (H, H2))
+    if q_start.dim() != 1 or q_start.shape[0] < 1:
+        raise ValueError("q_start must be [B + 1], got %s" % (tuple(q_start.shape),))
     B = q_start.shape[0] - 1
     dev = hidden.device
+    _expect(weight, "weight", None, hidden.dtype, dev)
+    _expect(tokens, "tokens", (T,), i32, dev)
+    _expect(q_start, "q_start", None, i32, dev)
+    for name, t, n in (("argmax_out", argmax_out, T), ("accept_len", accept_len, B),
+                       ("num_emitted", num_emitted, B), ("emitted", emitted, T)):
+        if t is not None:
+            _expect(t, name, (n,), i32, dev)
+    if workspace is not None:
+        _expect(workspace, "workspace", None, None, dev)
     code = _dtype_code(hidden)
     if argmax_out is None:
         argmax_out = torch.empty(T, dtype=i32, device=dev)
@@ -340,10 +414,17 @@ def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float
     with ctx_len, seq_lens.  ``out`` may hold preallocated tensors by name.
     """
     import torch
+    if cand_start.dim() != 1 or cand_start.shape[0] < 1 or cand_tokens.dim() != 2:
+        raise ValueError("cand_start must be [B + 1] and cand_tokens [C, max_len]")
     B = cand_start.shape[0] - 1
     C, max_len = cand_tokens.shape
     dev = cand_start.device
     i32 = torch.int32
+    _expect(cand_len, "cand_len", (C,), i32, dev)
+    _expect(cand_tokens, "cand_tokens", None, i32, dev)
+    _expect(last_token, "last_token", (B,), i32, dev)
+    if ctx_len is not None:
+        _expect(ctx_len, "ctx_len", (B,), i32, dev)
     o = dict(out or {})
     shapes = dict(score=(B, torch.float64), agree=(B, i32), prefix_len=(B, i32), source=(B, i32),
                   draft_len=(B, i32), q_start=(B + 1, i32), tokens=(B * (max_len + 1), i32))
@@ -352,6 +433,13 @@ def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float
     for k, (n, dt) in shapes.items():
         if k not in o:
             o[k] = torch.empty(max(n, 1) if k == "tokens" else n, dtype=dt, device=dev)
+        elif k == "tokens":
+            # the capacity is passed to the call, which checks it
+            _expect(o[k], k, None, dt, dev)
+            if o[k].dim() != 1:
+                raise ValueError("tokens must be one-dimensional")
+        else:
+            _expect(o[k], k, (n,), dt, dev)
     rc = library().verify_budget(
         B, C, max_len, _dev_ptr(cand_start, "cand_start", i32), _dev_ptr(cand_len, "cand_len", i32),
         _dev_ptr(cand_tokens, "cand_tokens", i32), _dev_ptr(last_token, "last_token", i32),
@@ -370,8 +458,16 @@ def verify_kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, q_s
     """Write the new tokens' K/V ([T, Hkv, D], the cache's dtype) into their
     paged-cache slots (position S_i - n_i + j for row j of request i), in place."""
     import torch
-    params = _attn_params(torch.empty((0, k_new.shape[1], k_new.shape[2]), dtype=k_new.dtype),
-                          k_cache, block_tables, 0, 0.0, 0)
+    if k_new.dim() != 3:
+        raise ValueError("k_new must be [T, Hkv, D], got %s" % (tuple(k_new.shape),))
+    _expect(v_new, "v_new", tuple(k_new.shape), k_new.dtype, k_new.device)
+    if q_start.dim() != 1 or q_start.shape[0] < 1:
+        raise ValueError("q_start must be [B + 1], got %s" % (tuple(q_start.shape),))
+    probe = torch.empty((0, k_new.shape[1], k_new.shape[2]), dtype=k_new.dtype, device=k_new.device)
+    _check_attention_tensors(probe, k_cache, v_cache, block_tables, seq_lens, q_start)
+    if k_cache.shape[1] != k_new.shape[1]:
+        raise ValueError("k_new has %d KV heads, the cache %d" % (k_new.shape[1], k_cache.shape[1]))
+    params = _attn_params(probe, k_cache, block_tables, 0, 0.0, 0)
     i32 = torch.int32
     rc = library().verify_kv_append(
         ctypes.byref(params), k_new.shape[0], _dev_ptr(k_new, "k_new"),

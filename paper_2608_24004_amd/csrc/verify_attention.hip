@@ -1146,6 +1146,8 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
         pl.split_blocks = std::max(1, sb);
         pl.max_splits = (int)((nb_max + pl.split_blocks - 1) / pl.split_blocks);
         pl.row_groups = (int)((rows + kValuRows - 1) / kValuRows);
+        // grid (splits, KV heads x row groups, requests): y is a 16-bit dimension
+        if ((int64_t)p->num_kv_heads * pl.row_groups > 65535) return VERIFY_EUNSUPPORTED;
         if (pl.max_splits > 1) {
             const size_t items = (size_t)total_q * p->num_q_heads * pl.max_splits;
             pl.part_o_bytes = align_up(items * p->head_dim * sizeof(float), 256);
@@ -1307,6 +1309,7 @@ extern "C" int verify_kv_append(const verify_attn_params* params, int32_t total_
     if (total_q == 0 || p.num_seqs == 0) return VERIFY_OK;
     if (!k_new || !v_new || !block_tables || !seq_lens || !q_start || !k_cache || !v_cache)
         return VERIFY_EINVAL;
+    if (p.num_kv_heads > 65535) return VERIFY_EUNSUPPORTED;  // grid y
     const dim3 grid((unsigned)total_q, (unsigned)p.num_kv_heads);
 #define AVERIFY_APPEND(T, D)                                                                       \
     hipLaunchKernelGGL((attn_kv_append<T, D>), grid, dim3(D), 0, stream, p.num_seqs, p.num_kv_heads, \

@@ -241,3 +241,62 @@ def test_kv_append_argument_validation():
     assert lib.verify_kv_append(ctypes.byref(_params()), -1, d, d, d, d, d, d, d, None) == av.EINVAL
     # nothing to append: a no-op that needs no pointers
     assert lib.verify_kv_append(ctypes.byref(_params()), 0, *([None] * 7), None) == 0
+
+
+def test_binding_checks_tensor_shapes_dtypes_and_devices():
+    """The binding refuses tensors whose sizes disagree with what the call
+    derives from the others (the kernels would index past them).  Meta
+    tensors carry shapes without storage, so every check runs without a GPU;
+    tensors that pass them stop at the device-memory check."""
+    import torch
+    m = dict(device="meta")
+    bf, i32 = torch.bfloat16, torch.int32
+    base = dict(q=torch.empty(36, 32, 128, dtype=bf, **m),
+                k_cache=torch.empty(100, 8, 16, 16, 8, dtype=bf, **m),
+                v_cache=torch.empty(100, 8, 128, 16, dtype=bf, **m),
+                block_tables=torch.empty(4, 30, dtype=i32, **m),
+                seq_lens=torch.empty(4, dtype=i32, **m), q_start=torch.empty(5, dtype=i32, **m))
+
+    def attn(**kw):
+        args = dict(base)
+        args.update(kw)
+        av.verify_attention(**args, max_q_len=9, max_seq_len=480)
+
+    with pytest.raises(ValueError, match="q must be a device tensor"):
+        attn()
+    with pytest.raises(ValueError, match="v_cache must have shape"):
+        attn(v_cache=torch.empty(100, 8, 128, 8, dtype=bf, **m))
+    with pytest.raises(ValueError, match="k_cache must have shape"):
+        attn(k_cache=torch.empty(100, 8, 8, 16, 16, dtype=bf, **m))
+    with pytest.raises(ValueError, match="q_start must have shape"):
+        attn(q_start=torch.empty(4, dtype=i32, **m))
+    with pytest.raises(TypeError, match="seq_lens must be"):
+        attn(seq_lens=torch.empty(4, dtype=torch.int64, **m))
+    with pytest.raises(ValueError, match="out must have shape"):
+        attn(out=torch.empty(35, 32, 128, dtype=bf, **m))
+    with pytest.raises(ValueError, match="sinks must have shape"):
+        attn(sinks=torch.empty(8, dtype=torch.float32, **m))
+    with pytest.raises(ValueError, match="block_tables is on cpu"):
+        attn(block_tables=torch.empty(4, 30, dtype=i32))
+
+    logits = torch.empty(36, 1000, dtype=bf, **m)
+    qs = torch.empty(5, dtype=i32, **m)
+    with pytest.raises(ValueError, match="tokens must have shape"):
+        av.verify_accept(logits, torch.empty(35, dtype=i32, **m), qs)
+    with pytest.raises(ValueError, match="emitted must have shape"):
+        av.verify_accept(logits, torch.empty(36, dtype=i32, **m), qs,
+                         emitted=torch.empty(30, dtype=i32, **m))
+    with pytest.raises(ValueError, match="accept_len must have shape"):
+        av.verify_accept_sampled(logits, torch.empty(36, dtype=i32, **m), qs, temperature=0.7, seed=1,
+                                 accept_len=torch.empty(5, dtype=i32, **m))
+    with pytest.raises(ValueError, match="tokens must have shape"):
+        av.verify_lmhead_accept(torch.empty(36, 64, dtype=bf, **m), torch.empty(1000, 64, dtype=bf, **m),
+                                torch.empty(30, dtype=i32, **m), qs)
+    with pytest.raises(ValueError, match="last_token must have shape"):
+        av.verify_budget(torch.empty(5, dtype=i32, **m), torch.empty(9, dtype=i32, **m),
+                         torch.empty(9, 16, dtype=i32, **m), torch.empty(3, dtype=i32, **m),
+                         alpha=64.0, g_min=0.3)
+    with pytest.raises(ValueError, match="v_new must have shape"):
+        av.verify_kv_append(torch.empty(36, 8, 128, dtype=bf, **m), torch.empty(36, 8, 64, dtype=bf, **m),
+                            base["k_cache"], base["v_cache"], base["block_tables"], base["seq_lens"],
+                            base["q_start"])
