@@ -218,6 +218,20 @@ def test_attention_split_invariance_and_degenerate():
         _check_paged(p, split=split, what="split=%d" % split)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64)])
+def test_attention_requests_without_rows(dtype, hq, hkv, d):
+    # requests with no scored row (n_i = 0, with and without cached keys)
+    # between ordinary ones: they get no work and leave the others unchanged
+    say("attn empty requests", dtype, hq, hkv, d)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                     contexts=[100, 50, 0, 700, 33, 0, 1200], drafts=[3, -1, 0, -1, 8, -1, 5],
+                     seed=hq + d)
+    assert (np.diff(p.q_start) == 0).sum() == 3
+    for split in (0, 1, 3):
+        _check_paged(p, split=split, what="empty requests split=%d" % split)
+
+
 @pytest.mark.parametrize("hq,hkv,d", [(64, 8, 64), (32, 8, 128), (16, 2, 64)])
 def test_attention_long_pairs(hq, hkv, d):
     # pairs of 64 blocks and more run on the one-wavefront shapes (72 rows at
