@@ -12,20 +12,29 @@
 from __future__ import annotations
 
 import math
+import os
 
 import numpy as np
 import pytest
 
 import oracle
 
-KAT = [  # counter words, key words, output words
-    ((0x00000000, 0x00000000, 0x00000000, 0x00000000), (0x00000000, 0x00000000),
-     (0x6627e8d5, 0xe169c58d, 0xbc57ac4c, 0x9b00dbd8)),
-    ((0xffffffff, 0xffffffff, 0xffffffff, 0xffffffff), (0xffffffff, 0xffffffff),
-     (0x408f276d, 0x41c83b0e, 0xa20bc7c6, 0x6d5451fd)),
-    ((0x243f6a88, 0x85a308d3, 0x13198a2e, 0x03707344), (0xa4093822, 0x299f31d0),
-     (0xd16cfe09, 0x94fdcceb, 0x5001e420, 0x24126ea1)),
-]
+def _load_kat():
+    """(counter, key, output) word tuples from tests/golden/philox4x32_10_kat.txt."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "philox4x32_10_kat.txt")
+    out = []
+    with open(path) as f:
+        for line in f:
+            line = line.split("#", 1)[0].split()
+            if not line:
+                continue
+            w = [int(x, 16) for x in line]
+            assert len(w) == 10, line
+            out.append((tuple(w[0:4]), tuple(w[4:6]), tuple(w[6:10])))
+    return out
+
+
+KAT = _load_kat()
 
 
 @pytest.mark.parametrize("ctr,key,want", KAT)
