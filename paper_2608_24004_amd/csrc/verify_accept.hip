@@ -66,9 +66,9 @@ __device__ __forceinline__ void scan_vec(const uint4& v, uint32_t base, float& b
 template <typename T>
 __global__ __launch_bounds__(kArgmaxThreads) void argmax_chunks(
     const T* __restrict__ logits, int64_t row_stride, int64_t vocab, int64_t chunk_elems,
-    int nchunks, uint64_t* __restrict__ partial) {
+    int nchunks, uint64_t* __restrict__ partial, int64_t row0) {
     constexpr int E = Storage<T>::kPer16B;
-    const int64_t row = blockIdx.y;
+    const int64_t row = row0 + blockIdx.y;
     const int c = blockIdx.x;
     const T* rowp = logits + row * row_stride;
     const int64_t lo = (int64_t)c * chunk_elems;
@@ -245,12 +245,12 @@ constexpr int kSampleUnroll = 2;         // 16-byte vectors per lane per iterati
 template <typename T>
 __global__ __launch_bounds__(kArgmaxThreads) void sample_chunks(
     const T* __restrict__ logits, int64_t row_stride, int64_t vocab, int64_t chunk_elems,
-    int nchunks, uint64_t* __restrict__ partial, SampleParams sp) {
+    int nchunks, uint64_t* __restrict__ partial, SampleParams sp, int64_t row0) {
     constexpr int E = Storage<T>::kPer16B;
     // queued logit: (x bits, code k, index, unused)
     __shared__ uint4 queue[kArgmaxThreads / kWave][kSampleQueue];
     __shared__ uint64_t red[kArgmaxThreads / kWave];
-    const int64_t row = blockIdx.y;
+    const int64_t row = row0 + blockIdx.y;
     const uint32_t urow = (uint32_t)row;
     const int c = blockIdx.x;
     const T* rowp = logits + row * row_stride;
@@ -516,25 +516,28 @@ int accept_launch(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_
     uint64_t* partial = static_cast<uint64_t*>(workspace);
     int32_t* am = argmax_out ? argmax_out
                              : reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + p.partial_bytes);
-    if (total_q > 0) {
-        dim3 grid(p.nchunks, total_q), block(kArgmaxThreads);
+    // rows go on grid y, at most 65535 per launch
+    constexpr int kRowsPerLaunch = 65535;
+    for (int64_t r0 = 0; r0 < total_q; r0 += kRowsPerLaunch) {
+        const dim3 grid(p.nchunks, (unsigned)std::min<int64_t>(kRowsPerLaunch, total_q - r0));
+        const dim3 block(kArgmaxThreads);
         const bool bf16 = logits_dtype == VERIFY_BF16;
         if (sp && bf16) {
             hipLaunchKernelGGL(sample_chunks<uint16_t>, grid, block, 0, stream,
                                static_cast<const uint16_t*>(logits), row_stride, vocab,
-                               p.chunk_elems, p.nchunks, partial, *sp);
+                               p.chunk_elems, p.nchunks, partial, *sp, r0);
         } else if (sp) {
             hipLaunchKernelGGL(sample_chunks<float>, grid, block, 0, stream,
                                static_cast<const float*>(logits), row_stride, vocab,
-                               p.chunk_elems, p.nchunks, partial, *sp);
+                               p.chunk_elems, p.nchunks, partial, *sp, r0);
         } else if (bf16) {
             hipLaunchKernelGGL(argmax_chunks<uint16_t>, grid, block, 0, stream,
                                static_cast<const uint16_t*>(logits), row_stride, vocab,
-                               p.chunk_elems, p.nchunks, partial);
+                               p.chunk_elems, p.nchunks, partial, r0);
         } else {
             hipLaunchKernelGGL(argmax_chunks<float>, grid, block, 0, stream,
                                static_cast<const float*>(logits), row_stride, vocab,
-                               p.chunk_elems, p.nchunks, partial);
+                               p.chunk_elems, p.nchunks, partial, r0);
         }
         if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
     }

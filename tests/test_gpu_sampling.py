@@ -170,3 +170,32 @@ def test_sampled_strided_rows():
     acc, ne, em = oracle.accept(q_start.cpu().numpy(), tokens.cpu().numpy(), y_ref)
     np.testing.assert_array_equal(outs[1].cpu().numpy(), acc)
     np.testing.assert_array_equal(outs[3].cpu().numpy(), em)
+
+
+def test_more_rows_than_one_launch_holds():
+    # 70 000 scored rows: the per-chunk kernels run in slices of at most 65 535
+    # rows (the grid's y limit); the draws depend on the absolute row index
+    rng = np.random.default_rng(70000)
+    n = np.full(7000, 10)
+    q_start = np.zeros(n.size + 1, dtype=np.int32)
+    q_start[1:] = np.cumsum(n)
+    V = 24
+    logits = torch.as_tensor(rng.standard_normal((int(q_start[-1]), V)).astype(np.float32)).to(
+        torch.bfloat16)
+    code = workload.dtype_code("bf16")
+    seed, offset = 1234567, 9
+    y_ref = oracle.sample(workload.host_storage(logits), code, 0.8, seed=seed, offset=offset)
+    tokens = _plant(y_ref, q_start, rng, V)
+    say("sampled 70000 rows")
+    want = _oracle_all(logits, q_start, tokens, code, 0.8, seed, offset)
+    d_logits, d_tok, d_qs = (logits.to(DEV), torch.as_tensor(tokens, device=DEV),
+                             torch.as_tensor(q_start, device=DEV))
+    _check(_gpu(d_logits, d_tok, d_qs, 0.8, seed, offset), want)
+    acc, ne, em, am = av.verify_accept(d_logits, d_tok, d_qs)
+    torch.cuda.synchronize()
+    am_ref, _ = oracle.argmax(workload.host_storage(logits), code, with_gap=False)
+    r_acc, r_ne, r_em = oracle.accept(q_start, tokens, am_ref)
+    np.testing.assert_array_equal(am.cpu().numpy(), am_ref)
+    np.testing.assert_array_equal(acc.cpu().numpy(), r_acc)
+    np.testing.assert_array_equal(ne.cpu().numpy(), r_ne)
+    np.testing.assert_array_equal(em.cpu().numpy(), r_em)
