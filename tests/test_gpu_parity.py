@@ -232,6 +232,22 @@ def test_attention_requests_without_rows(dtype, hq, hkv, d):
         _check_paged(p, split=split, what="empty requests split=%d" % split)
 
 
+@pytest.mark.parametrize("dtype,hq,hkv,d", [("bf16", 32, 8, 128), ("bf16", 8, 2, 64), ("f32", 8, 2, 64)])
+def test_attention_batches_above_the_inline_schedule(dtype, hq, hkv, d):
+    # more than 256 requests: the per-request unit offsets come from the
+    # separate one-workgroup schedule launch instead of each workgroup's scan
+    rng = np.random.default_rng(300 + d)
+    B = 300
+    contexts = rng.integers(0, 200, size=B)
+    drafts = rng.integers(0, 9, size=B)
+    drafts[::37] = -1          # a few requests without scored rows
+    say("attn 300 requests", dtype, hq, hkv, d)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                     contexts=contexts.tolist(), drafts=drafts.tolist(), seed=int(d))
+    for split in (0, 1, 3):
+        _check_paged(p, split=split, what="300 requests split=%d" % split)
+
+
 @pytest.mark.parametrize("hq,hkv,d", [(64, 8, 64), (32, 8, 128), (16, 2, 64)])
 def test_attention_long_pairs(hq, hkv, d):
     # pairs of 64 blocks and more run on the one-wavefront shapes (72 rows at
