@@ -182,6 +182,18 @@ def test_attention_every_draft_length(k):
     _check_paged(p, split=4)
 
 
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (16, 2)])
+@pytest.mark.parametrize("k", [0, 1, 3, 4, 5, 7, 8, 11, 12, 15, 16, 20, 24, 28, 31, 32])
+def test_attention_every_head_dim_64_shape(hq, hkv, k):
+    # head dim 64: the row count G (k + 1) walks every kernel shape of the
+    # table, one to seventeen 16-row tiles
+    say("attn d64 k", hq, hkv, k)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=64, dtype="bf16",
+                     contexts=[5, 100, 517, 1100], drafts=[k, k, k, k], seed=k + hq)
+    for split in (0, 4):
+        _check_paged(p, split=split, what="d64 k=%d split=%d" % (k, split))
+
+
 def test_attention_spiky_masks():
     # Large-norm queries and a planted key that matches them at a position just
     # after some rows: a causal or window leak changes those rows by O(1).
