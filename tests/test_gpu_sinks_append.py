@@ -101,3 +101,40 @@ def test_kv_append_matches_oracle_and_feeds_attention(dtype, hq, hkv, d):
     args.update(k_cache=kc_ref, v_cache=vc_ref)
     ref = oracle.attention(**args)
     assert_attention_close(got, ref, dtype, "after append")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_kv_append_skips_rows_without_a_slot(dtype):
+    # rows whose position is negative (S < n), lies past the block table, or
+    # maps to a block id outside [0, num_blocks) write nothing; every other
+    # row lands in its slot, bit for bit as in the oracle
+    hq, hkv, d = 16, 4, 64
+    say("append skips", dtype)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                     contexts=[40, 100, 20, 64], drafts=[7, 3, 9, 4], seed=11)
+    bt = p.block_tables.copy()
+    sl = p.seq_lens.copy()
+    bt[0, 2] = -1                       # positions 32..47 of request 0: no block
+    bt[1, 1] = p.num_blocks + 5         # positions 16..31 of request 1: id out of range
+    sl[2] = 5                           # request 2: 10 rows but only 5 keys, p < 0 for 5 rows
+    sl[3] = bt.shape[1] * 16 + 3        # request 3: its last rows fall past the block table
+    T = p.total_q
+    tdt = workload.torch_dtype(dtype)
+    g = torch.Generator().manual_seed(5)
+    k_new = torch.randn((T, hkv, d), generator=g).to(tdt)
+    v_new = torch.randn((T, hkv, d), generator=g).to(tdt)
+    code = workload.dtype_code(dtype)
+    kc_ref, vc_ref = oracle.kv_append(num_kv_heads=hkv, head_dim=d, dtype=code,
+                                      k_new=workload.host_storage(k_new),
+                                      v_new=workload.host_storage(v_new),
+                                      block_tables=bt, seq_lens=sl, q_start=p.q_start,
+                                      k_cache=workload.host_storage(p.k_cache),
+                                      v_cache=workload.host_storage(p.v_cache))
+    kc, vc = p.k_cache.to(DEV), p.v_cache.to(DEV)
+    av.verify_kv_append(k_new.to(DEV), v_new.to(DEV), kc, vc, torch.as_tensor(bt, device=DEV),
+                        torch.as_tensor(sl, device=DEV), torch.as_tensor(p.q_start, device=DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(workload.host_storage(kc), kc_ref)
+    assert np.array_equal(workload.host_storage(vc), vc_ref)
+    # something was skipped and something was written
+    assert not np.array_equal(kc_ref, workload.host_storage(p.k_cache))
