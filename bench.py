@@ -361,7 +361,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the verify step runs on a single MI355X "
-              "(--gpus %d requested; multi-GPU sharding is not part of this build)" % args.gpus,
+              "(--gpus %d requested; the verify step here runs and is measured on one GPU)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
 

@@ -68,7 +68,7 @@ extern "C" {
 enum verify_status {
     VERIFY_OK = 0,
     VERIFY_EINVAL = -1,       /* null pointer, negative size, inconsistent arguments   */
-    VERIFY_EUNSUPPORTED = -2, /* head_dim, block_size or dtype this build does not handle,
+    VERIFY_EUNSUPPORTED = -2, /* head_dim, block_size or dtype this library does not handle,
                                  or sizes beyond a launch grid's limits                 */
     VERIFY_EWORKSPACE = -3,   /* workspace smaller than the size query returned        */
     VERIFY_EHIP = -4          /* a kernel launch failed (hipGetLastError)               */
