@@ -127,7 +127,10 @@ __device__ __forceinline__ void lds_barrier() {
 // global_load_lds_dwordx4): lane l of the wavefront writes LDS bytes
 // [lds + 16 l, lds + 16 l + 16).  The load is issued from inline assembly so
 // that its completion is tracked by the pipeline's explicit waits alone; the
-// compiler does not see it and adds no waits of its own.
+// compiler does not see it and adds no waits of its own.  m0 (the LDS base of
+// the copy) is set inside the same statement and listed as clobbered; nothing
+// else in these kernels uses m0 (no LDS-direct, movrel or message
+// instructions), so no value of the compiler's lives in it across the copy.
 __device__ __forceinline__ void dma16(uint32_t lds_wave_base, const void* src) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                  :
