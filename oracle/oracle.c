@@ -479,38 +479,45 @@ int oracle_budget(int32_t num_seqs, int32_t max_len, const int32_t *cand_start,
     for (int i = 0; i < num_seqs; ++i) {
         const int32_t r0 = cand_start[i], n = cand_start[i + 1] - r0;
         score[i] = 0.0; agree[i] = 0; prefix_len[i] = 0; source[i] = -1;
-        /* The prefixes starting with one first token are all shared by at most
-         * the candidates of that first token; the group's longest common prefix
-         * is shared by all of them.  So the most frequent prefix is the longest
-         * common prefix of the largest first-token group. */
-        int32_t best_c = 0, best_l = 0, best_tok = 0, best_row = -1;
+        /* Every non-empty prefix of every candidate, counted by its definition:
+         * prefix (a, l) -- the first l tokens of candidate a -- is shared by
+         * the candidates b whose common prefix with a is at least l tokens.
+         * The most frequent prefix wins; equally frequent ones go to the
+         * longer, then to the lexicographically smaller token sequence. */
+        int32_t best_c = 0, best_l = 0, best_row = -1;
         for (int32_t a = 0; a < n; ++a) {
-            const int32_t ra = r0 + a;
-            if (cand_len[ra] <= 0) continue;
+            const int32_t ra = r0 + a, la = cand_len[ra];
+            if (la <= 0) continue;
             const int32_t *ta = cand_tokens + (int64_t)ra * max_len;
-            int32_t c = 0, l = cand_len[ra];
-            for (int32_t b = 0; b < n; ++b) {
-                const int32_t rb = r0 + b;
-                if (cand_len[rb] <= 0) continue;
-                const int32_t *tb = cand_tokens + (int64_t)rb * max_len;
-                if (tb[0] != ta[0]) continue;
-                ++c;
-                const int k = common_prefix(ta, cand_len[ra], tb, cand_len[rb]);
-                if (k < l) l = k;
-            }
-            if (c > best_c || (c == best_c && (l > best_l || (l == best_l && ta[0] < best_tok)))) {
-                best_c = c; best_l = l; best_tok = ta[0]; best_row = ra;
+            for (int32_t l = 1; l <= la; ++l) {
+                int32_t c = 0;
+                for (int32_t b = 0; b < n; ++b) {
+                    const int32_t rb = r0 + b;
+                    if (cand_len[rb] < l) continue;
+                    if (common_prefix(ta, l, cand_tokens + (int64_t)rb * max_len, l) == l) ++c;
+                }
+                int better = c > best_c || (c == best_c && l > best_l);
+                if (!better && c == best_c && l == best_l && best_row >= 0) {
+                    const int32_t *tb = cand_tokens + (int64_t)best_row * max_len;
+                    int32_t k = 0;
+                    while (k < l && ta[k] == tb[k]) ++k;
+                    better = k < l && ta[k] < tb[k];
+                }
+                if (better) { best_c = c; best_l = l; best_row = ra; }
             }
         }
         if (best_c == 0) continue;
-        /* drafts come from the longest candidate of the group (lowest row on ties) */
+        /* drafts come from the longest candidate starting with the prefix
+         * (lowest row on ties) */
+        const int32_t *pref = cand_tokens + (int64_t)best_row * max_len;
         int32_t src = -1;
         for (int32_t b = 0; b < n; ++b) {
             const int32_t rb = r0 + b;
-            if (cand_len[rb] <= 0 || cand_tokens[(int64_t)rb * max_len] != best_tok) continue;
+            if (cand_len[rb] < best_l) continue;
+            if (common_prefix(pref, best_l, cand_tokens + (int64_t)rb * max_len, best_l) != best_l)
+                continue;
             if (src < 0 || cand_len[rb] > cand_len[src]) src = rb;
         }
-        (void)best_row;
         const double p = g_min + (1.0 - g_min) * (1.0 - exp(1.0 - (double)n));
         score[i] = ((double)best_c / (double)n) * p;
         agree[i] = best_c;
