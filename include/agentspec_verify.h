@@ -187,6 +187,32 @@ int verify_accept(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_
                   size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * verify_accept_noalloc -- verify_accept for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  It takes no workspace; its scratch (the
+ * per-(row, chunk) maxima and, when argmax_out is NULL, the argmax) lives in
+ * a device array of VERIFY_NOALLOC_SCRATCH_BYTES that the library holds on
+ * each GPU it runs on until the process ends.  The call itself allocates
+ * nothing.
+ *
+ * Arguments, outputs and results are verify_accept's (bit-identical).
+ * VERIFY_EWORKSPACE (nothing enqueued) if verify_accept_workspace_size() for
+ * the same (num_seqs, total_q, vocab, logits_dtype) exceeds
+ * VERIFY_NOALLOC_SCRATCH_BYTES; with bf16 logits that holds up to about
+ * 340 000 rows.  VERIFY_EHIP if the scratch's device address cannot be
+ * obtained.
+ * All calls on one GPU share its scratch: calls that overlap on one GPU (on
+ * different streams, or from different host threads without ordering) race
+ * and may return wrong results.  Calls on one stream are ordered and safe.
+ */
+#define VERIFY_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+int verify_accept_noalloc(int32_t num_seqs, int32_t total_q, int64_t vocab, int64_t row_stride,
+                          int32_t logits_dtype, const void *logits, const int32_t *tokens,
+                          const int32_t *q_start, int32_t *argmax_out, int32_t *accept_len,
+                          int32_t *num_emitted, int32_t *emitted, hipStream_t stream);
+
+/*
  * verify_accept_sampled -- stochastic verification at temperature T > 0
  * (Sec. 2.2: the speculative output follows the target's distribution).
  *

@@ -19,11 +19,13 @@ from typing import Optional
 
 from .build import LIB_PATH
 
-__all__ = ["verify_attention", "verify_accept", "verify_accept_sampled", "verify_lmhead_accept",
+__all__ = ["verify_attention", "verify_accept", "verify_accept_noalloc", "verify_accept_sampled",
+           "verify_lmhead_accept",
            "verify_budget", "verify_kv_append", "attention_workspace_size", "accept_workspace_size",
            "lmhead_accept_workspace_size", "VerifyError", "library", "abi_version", "F32", "BF16"]
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+NOALLOC_SCRATCH_BYTES = 4 << 20  # VERIFY_NOALLOC_SCRATCH_BYTES of the C header
 F32, BF16 = 0, 1
 
 
@@ -74,6 +76,8 @@ def library(path: Optional[str] = None):
     lib.verify_accept_workspace_size.restype = ctypes.c_int
     lib.verify_accept.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.verify_accept.restype = ctypes.c_int
+    lib.verify_accept_noalloc.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.verify_accept_noalloc.restype = ctypes.c_int
     lib.verify_accept_sampled.argtypes = [i32, i32, i64, i64, i32, vp, vp, vp, ctypes.c_float,
                                           ctypes.c_uint64, ctypes.c_uint32, vp, vp, vp, vp, vp, sz, vp]
     lib.verify_accept_sampled.restype = ctypes.c_int
@@ -256,7 +260,8 @@ def accept_workspace_size(num_seqs: int, total_q: int, vocab: int, dtype_code: i
     return int(n.value)
 
 
-def _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace):
+def _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace,
+                    need_workspace=True):
     import torch
     if logits.dim() != 2:
         raise ValueError("logits must be [T, V], got %s" % (tuple(logits.shape),))
@@ -282,7 +287,7 @@ def _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitte
         num_emitted = torch.empty(B, dtype=i32, device=dev)
     if emitted is None:
         emitted = torch.empty(T, dtype=i32, device=dev)
-    ws_bytes = accept_workspace_size(B, T, V, code)
+    ws_bytes = accept_workspace_size(B, T, V, code) if need_workspace else 0
     if workspace is None and ws_bytes > 0:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     ws_have = workspace.numel() * workspace.element_size() if workspace is not None else 0
@@ -308,6 +313,28 @@ def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, 
         _dev_ptr(emitted, "emitted", i32), _dev_ptr(workspace, "workspace"), ws_have,
         _stream_ptr(stream, logits.device))
     _check(rc, "verify_accept")
+    return accept_len, num_emitted, emitted, argmax_out
+
+
+def verify_accept_noalloc(logits, tokens, q_start, *, argmax_out=None, accept_len=None,
+                          num_emitted=None, emitted=None, stream=None):
+    """verify_accept without a workspace: the library's per-GPU scratch array
+    holds the partial maxima (for callers that cannot allocate; calls that
+    overlap on one GPU race).  Outputs not passed in are allocated here, by
+    torch, before the call; the C call allocates nothing.  Returns
+    (accept_len [B], num_emitted [B], emitted [T], argmax [T])."""
+    import torch
+    i32 = torch.int32
+    B, T, V, code, argmax_out, accept_len, num_emitted, emitted, _, _ = \
+        _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, None,
+                        need_workspace=False)
+    _expect(tokens, "tokens", (T,), i32, logits.device)
+    rc = library().verify_accept_noalloc(
+        B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
+        _dev_ptr(q_start, "q_start", i32), _dev_ptr(argmax_out, "argmax_out", i32),
+        _dev_ptr(accept_len, "accept_len", i32), _dev_ptr(num_emitted, "num_emitted", i32),
+        _dev_ptr(emitted, "emitted", i32), _stream_ptr(stream, logits.device))
+    _check(rc, "verify_accept_noalloc")
     return accept_len, num_emitted, emitted, argmax_out
 
 

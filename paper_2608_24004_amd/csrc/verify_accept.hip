@@ -15,7 +15,16 @@
 //                  partials to the row argmax, then finds the first draft
 //                  that disagrees (wavefront ballot) and writes the accepted
 //                  drafts and the bonus token.
+#include <atomic>
+#include <mutex>
+
 #include "common.h"
+
+// Scratch of verify_accept_noalloc (the per-(row, chunk) maxima, then the
+// argmax when the caller passes none): one copy per GPU, held until the
+// process ends.  In host code this name is not a device address; the
+// address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint8_t scratch[VERIFY_NOALLOC_SCRATCH_BYTES];
 
 namespace averify {
 namespace {
@@ -603,4 +612,52 @@ extern "C" int verify_accept_sampled(int32_t num_seqs, int32_t total_q, int64_t 
     return accept_launch(num_seqs, total_q, vocab, row_stride, logits_dtype, logits, tokens, q_start,
                          sampled_out, accept_len, num_emitted, emitted, workspace, workspace_bytes,
                          &sp, stream);
+}
+
+// Device address of `scratch` on the current device, looked up on the first
+// call per device (with that device current) and kept.
+static int noalloc_scratch(void** out) {
+    static std::atomic<void*> ptrs[64];
+    static std::mutex mu;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return VERIFY_EHIP;
+    }
+    if (dev < 0 || dev >= 64) return VERIFY_EUNSUPPORTED;
+    void* p = ptrs[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(mu);
+        p = ptrs[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+                (void)hipGetLastError();
+                return VERIFY_EHIP;
+            }
+            ptrs[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return VERIFY_OK;
+}
+
+extern "C" int verify_accept_noalloc(int32_t num_seqs, int32_t total_q, int64_t vocab,
+                                     int64_t row_stride, int32_t logits_dtype, const void* logits,
+                                     const int32_t* tokens, const int32_t* q_start,
+                                     int32_t* argmax_out, int32_t* accept_len,
+                                     int32_t* num_emitted, int32_t* emitted, hipStream_t stream) {
+    // sizes first: a call the scratch cannot hold fails before any HIP call
+    if (logits_dtype != VERIFY_F32 && logits_dtype != VERIFY_BF16) return VERIFY_EUNSUPPORTED;
+    if (!accept_args_ok(num_seqs, total_q, vocab, logits_dtype)) return VERIFY_EINVAL;
+    const AcceptPlan p = plan_accept(total_q, vocab, logits_dtype);
+    const size_t need = p.partial_bytes + p.argmax_bytes;
+    if (need > (size_t)VERIFY_NOALLOC_SCRATCH_BYTES) return VERIFY_EWORKSPACE;
+    void* ws = nullptr;
+    const int rc = noalloc_scratch(&ws);
+    if (rc != VERIFY_OK) return rc;
+    // every partial the scan reads is written by the argmax pass of the same
+    // call, so nothing of the previous call's contents needs clearing
+    return accept_launch(num_seqs, total_q, vocab, row_stride, logits_dtype, logits, tokens, q_start,
+                         argmax_out, accept_len, num_emitted, emitted, ws,
+                         (size_t)VERIFY_NOALLOC_SCRATCH_BYTES, nullptr, stream);
 }

@@ -28,7 +28,7 @@ def test_header_declares_the_entry_points():
     names = declared_symbols()
     for n in ("verify_attention", "verify_accept", "verify_accept_sampled", "verify_budget",
               "verify_kv_append", "verify_attention_workspace_size",
-              "verify_accept_workspace_size", "verify_lmhead_accept",
+              "verify_accept_workspace_size", "verify_lmhead_accept", "verify_accept_noalloc",
               "verify_lmhead_accept_workspace_size", "verify_status_string", "verify_abi_version"):
         assert n in names
 
@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10300
+    assert av.abi_version() == 10400
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
@@ -142,6 +142,28 @@ def test_accept_argument_validation():
     assert lib.verify_accept(4, 40, 100, 0, av.F32, *args, dummy, n.value - 1, None) == av.EWORKSPACE
     # empty batch is a no-op
     assert lib.verify_accept(0, 0, 100, 0, av.F32, *([None] * 8), 0, None) == 0
+
+
+def test_accept_noalloc_limits_checked_before_any_device_call():
+    """verify_accept_noalloc rejects, on the host, a call whose scratch need
+    exceeds the fixed per-GPU array, and bad arguments, before touching HIP."""
+    lib = av.library()
+    n = ctypes.c_size_t(0)
+    dummy = ctypes.c_void_p(0x1000)
+    # the largest bf16 row count the scratch holds, and one beyond it
+    fits, over = 0, 0
+    for rows in (100_000, 300_000, 400_000, 600_000):
+        assert lib.verify_accept_workspace_size(4, rows, 151936, av.BF16, ctypes.byref(n)) == 0
+        if n.value <= av.NOALLOC_SCRATCH_BYTES:
+            fits = rows
+        elif not over:
+            over = rows
+    assert fits >= 300_000 and over
+    assert lib.verify_accept_noalloc(4, over, 151936, 0, av.BF16, *([dummy] * 7), None) == \
+        av.EWORKSPACE
+    assert lib.verify_accept_noalloc(4, 40, 151936, 0, 7, *([dummy] * 7), None) == av.EUNSUPPORTED
+    assert lib.verify_accept_noalloc(4, 40, 0, 0, av.BF16, *([dummy] * 7), None) == av.EINVAL
+    assert lib.verify_accept_noalloc(-1, 40, 100, 0, av.F32, *([dummy] * 7), None) == av.EINVAL
 
 
 def test_accept_sampled_argument_validation():
