@@ -1,17 +1,22 @@
 """Throughput of the batched speculative-verification step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3_8b]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config qwen3_8b] [--seeds 0,1,2,3,4]
 
 One step = every attention layer of the workload (verify_attention) followed by
 verify_accept (vocabulary argmax + greedy acceptance) over one batch of
-synthetic inputs already resident in HBM.  Prints one JSON line:
+synthetic inputs already resident in HBM.  Every seed draws its own batch; per
+seed, W untimed steps, then K steps back to back with a HIP event between
+consecutive steps.  Prints one JSON line:
 
-  value         verified tokens/s = sum_i (accept_len_i + 1) / step time
+  value         verified tokens/s: per seed sum_i (accept_len_i + 1) / the
+                median step time, then the mean over seeds
   roofline      the attention call: algorithmic bytes per launch / mean launch
                 time (K calls back to back on the launch stream between two HIP
-                events, after the timed steps) vs 8 TB/s HBM
-  cpu_baseline  the CPU oracle on a bounded sample of the same step (first
-                requests of the batch, all their heads and logits rows)
+                events, after the timed steps; mean over seeds) vs 8 TB/s HBM,
+                and the same-run ceilings of a torch gather of the walk's K/V
+                tiles and of a plain device copy
+  cpu_baseline  the CPU oracle on a bounded sample of the first seed's step
+                (first requests of the batch, all their heads and logits rows)
 """
 from __future__ import annotations
 
@@ -170,7 +175,9 @@ def graph_time_us(fn, steps: int) -> float:
 def kv_append_timing(av, bt, steps: int):
     """Device time of writing the step's new tokens' K/V ([T, Hkv, D] each)
     into the first layer's cache (verify_kv_append), and its bytes: the new
-    K/V read once and written once."""
+    K/V read once and written once.  The calls rotate over enough copies of
+    the new K/V (more than the 256 MB Infinity Cache holds) that every call
+    reads its inputs from HBM."""
     import torch
     cfg = bt.cfg
     l = bt.layers[0]
@@ -179,43 +186,138 @@ def kv_append_timing(av, bt, steps: int):
     g.manual_seed(5)
     k_new = torch.randn((T, cfg.num_kv_heads, cfg.head_dim), generator=g, device=l.q.device).to(l.q.dtype)
     v_new = torch.randn_like(k_new)
-    # the cache is modified in place: append into copies of the touched blocks' cache
+    one = 2 * k_new.numel() * k_new.element_size()
+    copies = max(2, -(-(640 << 20) // one))
+    ks = [k_new.clone() for _ in range(copies)]
+    vs = [v_new.clone() for _ in range(copies)]
+    # the cache is modified in place: append into copies of the cache
     kc, vc = l.k_cache.clone(), l.v_cache.clone()
-    fn = lambda: av.verify_kv_append(k_new, v_new, kc, vc, bt.t_block_tables, bt.t_seq_lens,
-                                     bt.t_q_start)
+    it = [0]
+
+    def fn():
+        c = it[0] % copies
+        it[0] += 1
+        av.verify_kv_append(ks[c], vs[c], kc, vc, bt.t_block_tables, bt.t_seq_lens, bt.t_q_start)
     fn()
-    us = graph_time_us(fn, steps)
-    nbytes = 2 * 2 * k_new.numel() * k_new.element_size()
-    del kc, vc
-    return {"us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rows": T}
+    us = graph_time_us(fn, max(steps, 2 * copies))
+    nbytes = 2 * one
+    del kc, vc, ks, vs
+    return {"us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rows": T,
+            "input_copies": copies}
 
 
 def accept_timing(av, bt, steps: int, aws):
     """Device time of the acceptance calls on the step's logits: greedy
     (verify_accept) and stochastic at T = 0.7 (verify_accept_sampled), with
-    the logits' bytes per microsecond each reaches.  The sampled call scores
-    every logit with its own Gumbel noise, so it is bound by vector ALU work,
-    not by HBM."""
+    the logits' bytes per microsecond each reaches.  The calls rotate over
+    copies of the logits totalling more than twice the 256 MB Infinity Cache,
+    so that every call streams its logits from HBM, as in the step.  The
+    sampled call scores every logit with its own Gumbel noise, so it is bound
+    by vector ALU work, not by HBM."""
     import torch
     T, V = bt.logits.shape
     dev = bt.logits.device
     B = len(bt.q_start) - 1
+    nbytes = T * V * bt.logits.element_size()
+    copies = max(2, -(-(640 << 20) // max(1, nbytes)))
+    lg = [bt.logits] + [bt.logits.clone() for _ in range(copies - 1)]
     outs = [torch.empty(n, dtype=torch.int32, device=dev) for n in (B, B, T, T)]
-    greedy = lambda: av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start, accept_len=outs[0],
+    it = [0]
+
+    def nxt():
+        c = it[0] % copies
+        it[0] += 1
+        return lg[c]
+    greedy = lambda: av.verify_accept(nxt(), bt.t_tokens, bt.t_q_start, accept_len=outs[0],
                                       num_emitted=outs[1], emitted=outs[2], argmax_out=outs[3],
                                       workspace=aws)
-    sampled = lambda: av.verify_accept_sampled(bt.logits, bt.t_tokens, bt.t_q_start, temperature=0.7,
+    sampled = lambda: av.verify_accept_sampled(nxt(), bt.t_tokens, bt.t_q_start, temperature=0.7,
                                                seed=1234, offset=1, accept_len=outs[0],
                                                num_emitted=outs[1], emitted=outs[2],
                                                sampled_out=outs[3], workspace=aws)
-    nbytes = T * V * bt.logits.element_size()
-    res = {"logits_bytes": nbytes, "rows": T, "vocab": V}
+    res = {"logits_bytes": nbytes, "rows": T, "vocab": V, "logits_copies": copies}
     for name, fn in (("greedy", greedy), ("sampled_T0.7", sampled)):
         fn()
-        us = graph_time_us(fn, steps)
+        us = graph_time_us(fn, max(steps, 2 * copies))
         res[name] = {"us": us, "GBps": nbytes / (us * 1e-6) / 1e9,
                      "logits_per_ns": T * V / (us * 1e3)}
+    del lg
     return res
+
+
+def walk_tiles(bt, layer):
+    """(block, KV head) tile ids of every K/V tile one attention call walks,
+    request by request, head by head, block by block (visible blocks only)."""
+    import numpy as np
+    cfg = bt.cfg
+    Hkv = cfg.num_kv_heads
+    ids = []
+    n = np.diff(bt.q_start)
+    for i in range(len(bt.seq_lens)):
+        S = int(bt.seq_lens[i])
+        lo = 0 if layer.window == 0 else max(0, S - int(n[i]) - layer.window + 1)
+        blocks = bt.block_tables[i, lo // 16:(S + 15) // 16].astype(np.int64)
+        blocks = blocks[blocks >= 0]
+        for g in range(Hkv):
+            ids.append(blocks * Hkv + g)
+    return np.concatenate(ids) if ids else np.zeros(0, np.int64)
+
+
+def ceilings(bt, layer, reps: int = 10):
+    """Same-run bandwidth ceilings of the attention call's access pattern:
+    a torch index_select gather of every K and V tile the call walks (4 KiB
+    tiles at D 128 bf16, through the block table, in the walk's order), and a
+    plain device-to-device copy of 2 GiB.  Both count bytes read plus bytes
+    written; each is the mean over `reps` back-to-back calls."""
+    import torch
+    dev = layer.q.device
+    tile = layer.k_cache[0, 0].numel()
+    ktiles = layer.k_cache.view(-1, tile)
+    vtiles = layer.v_cache.view(-1, tile)
+    idx = torch.as_tensor(walk_tiles(bt, layer), device=dev)
+    ko = torch.empty((idx.numel(), tile), dtype=ktiles.dtype, device=dev)
+    vo = torch.empty_like(ko)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / reps
+
+    t = timed(lambda: (torch.index_select(ktiles, 0, idx, out=ko),
+                       torch.index_select(vtiles, 0, idx, out=vo)))
+    gbytes = 2.0 * 2 * ko.numel() * ko.element_size()
+    del ko, vo
+    src = torch.empty(1 << 30, dtype=torch.bfloat16, device=dev)
+    src.fill_(1.0)
+    dst = torch.empty_like(src)
+    tc = timed(lambda: dst.copy_(src))
+    cbytes = 2.0 * src.numel() * src.element_size()
+    del src, dst
+    return {"gather_GBps": gbytes / t / 1e9, "gather_bytes": gbytes,
+            "copy_GBps": cbytes / tc / 1e9, "copy_bytes": cbytes}
+
+
+def host_info():
+    """CPU model and host RAM of this machine (for the CPU baseline)."""
+    model, ram = None, None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal:"):
+                ram = round(int(line.split()[1]) * 1024 / 1e9, 1)
+                break
+    except OSError:
+        pass
+    return model, ram
 
 
 def lmhead_timing(av, workload, bt, steps: int):
@@ -330,10 +432,96 @@ def cpu_baseline(bt, budget_s: float):
             break
     passes.sort()
     value, done, elapsed = passes[len(passes) // 2]
+    model, ram = host_info()
     return dict(value=value, unit="verified tokens/s", cores=oracle.num_threads(), kind="oracle",
+                cpu_model=model, host_ram_GB=ram,
                 sample="%d of %d requests (all %d heads, %d layer(s), their logits rows); "
                        "median of %d pass(es), %.2f s per pass" % (
                            done, B, cfg.num_q_heads, len(bt.layers), len(passes), elapsed))
+
+
+def summarize_trace(csv_path: str, layers: int) -> None:
+    """Inter-kernel idle time inside the timed verify steps, from the kernel
+    trace of a rocprofv3 --kernel-trace run of bench.py.  A step is the
+    sequence (attn_persist, attn_combine_slots) x layers, argmax_chunks,
+    accept_scan issued back to back; every such run of steps in the trace is
+    used (the timed steps and the warm-up steps have this form; the
+    attention-only calls timed after them do not)."""
+    import collections
+    import csv
+    import re
+    import statistics as st
+    rows = []
+    for r in csv.DictReader(open(csv_path)):
+        m = re.search(r"averify::\(anonymous namespace\)::(\w+)", r["Kernel_Name"])
+        name = m.group(1) if m else "other"
+        rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), name))
+    rows.sort()
+    sig = ["attn_persist", "attn_combine_slots"] * layers + ["argmax_chunks", "accept_scan"]
+    steps = []
+    i = 0
+    while i + len(sig) <= len(rows):
+        if [x[2] for x in rows[i:i + len(sig)]] == sig:
+            steps.append(rows[i:i + len(sig)])
+            i += len(sig)
+        else:
+            i += 1
+    if not steps:
+        raise SystemExit("no verify step found in %s" % csv_path)
+    dur = collections.defaultdict(list)
+    gaps = collections.defaultdict(list)
+    spans, busy, between = [], [], []
+    for k, stp in enumerate(steps):
+        for j, (t0, t1, n) in enumerate(stp):
+            dur["%d %s" % (j, n)].append((t1 - t0) / 1e3)
+            if j:
+                gaps["%s -> %s" % (stp[j - 1][2], n)].append((t0 - stp[j - 1][1]) / 1e3)
+        spans.append((stp[-1][1] - stp[0][0]) / 1e3)
+        busy.append(sum(t1 - t0 for t0, t1, _ in stp) / 1e3)
+        if k and steps[k - 1][-1][1] <= stp[0][0] and stp[0][0] - steps[k - 1][-1][1] < 100e3:
+            between.append((stp[0][0] - steps[k - 1][-1][1]) / 1e3)
+    print("steps found: %d (kernel sequence %s)" % (len(steps), ", ".join(sig)))
+    print("")
+    print("| in-step kernel | median us |")
+    print("|---|---|")
+    for k in sorted(dur, key=lambda x: int(x.split()[0])):
+        print("| %s | %.1f |" % (k.split(" ", 1)[1], st.median(dur[k])))
+    print("")
+    print("| idle gap | median us |")
+    print("|---|---|")
+    for k, v in gaps.items():
+        print("| %s | %.2f |" % (k, st.median(v)))
+    if between:
+        print("| accept_scan -> next step's attn_persist | %.2f |" % st.median(between))
+    print("")
+    print("median step span %.1f us, of which kernels busy %.1f us, idle %.1f us" % (
+        st.median(spans), st.median(busy), st.median([a - b for a, b in zip(spans, busy)])))
+
+
+def summarize_counters(paths) -> None:
+    """Mean per dispatch of every counter of rocprofv3 --pmc runs, per kernel of
+    this library (KiB counters as read, before any calibration)."""
+    import collections
+    import csv
+    import re
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    for p in paths:
+        per = collections.defaultdict(float)
+        names = {}
+        for r in csv.DictReader(open(p)):
+            m = re.search(r"averify::\(anonymous namespace\)::(\w+)", r["Kernel_Name"])
+            if not m:
+                continue
+            key = (r["Dispatch_Id"], r["Counter_Name"])
+            per[key] += float(r["Counter_Value"])
+            names[r["Dispatch_Id"]] = m.group(1)
+        for (d, c), v in per.items():
+            agg[names[d]][c].append(v)
+    for k in sorted(agg):
+        print("%s:" % k)
+        for c in sorted(agg[k]):
+            v = agg[k][c]
+            print("  %-28s %16.1f  (mean of %d dispatches)" % (c, sum(v) / len(v), len(v)))
 
 
 def main():
@@ -342,9 +530,12 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="qwen3_8b")
-    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--seeds", default="0,1,2,3,4",
+                    help="comma-separated seeds; each draws its own batch (default: five)")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--side", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the other entry points and the same-run ceilings")
     ap.add_argument("--graph", action=argparse.BooleanOptionalAction, default=False,
                     help="replay the step as one captured HIP graph instead of launching its "
                          "kernels one by one (measured slower on this step)")
@@ -353,10 +544,18 @@ def main():
                          "and writes %d MiB (scale for the HBM byte counters)" % (CALIB_BYTES >> 20))
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the HBM traffic summary of two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print the in-step kernel times and idle gaps of a rocprofv3 "
+                         "--kernel-trace run and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="COUNTER_CSV",
+                    help="print per-kernel means of rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
 
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.config)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -365,106 +564,144 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    import workload
+    cfg = workload.CONFIGS[args.config]
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, len(cfg.windows))
+        return
+
+    import statistics
     import numpy as np
     import torch
     import paper_2608_24004_amd as av
-    import workload
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    cfg = workload.CONFIGS[args.config]
-    log("config", cfg.name, "seed", args.seed)
-    bt = workload.make_batch(cfg, args.seed, dev)
-    torch.cuda.synchronize()
-
+    seeds = [int(x) for x in args.seeds.split(",") if x.strip()]
     lib = av.library()
     stream = torch.cuda.current_stream()
-    outs = [torch.empty_like(l.q) for l in bt.layers]
-    ws = []
-    for l in bt.layers:
-        nb = av.attention_workspace_size(l.q, l.k_cache, bt.t_block_tables, max_q_len=bt.max_q_len,
-                                         max_seq_len=bt.max_seq_len, sliding_window=l.window)
-        ws.append(torch.empty(max(nb, 1), dtype=torch.uint8, device=dev))
-    T, B = bt.total_q, len(bt.seq_lens)
-    acc = torch.empty(B, dtype=torch.int32, device=dev)
-    ne = torch.empty(B, dtype=torch.int32, device=dev)
-    em = torch.empty(T, dtype=torch.int32, device=dev)
-    am = torch.empty(T, dtype=torch.int32, device=dev)
     code = workload.dtype_code(cfg.dtype)
-    aws = torch.empty(max(1, av.accept_workspace_size(B, T, cfg.vocab, code)), dtype=torch.uint8,
-                      device=dev)
-
-    def attention(li, ev=None):
-        l = bt.layers[li]
-        av.verify_attention(l.q, l.k_cache, l.v_cache, bt.t_block_tables, bt.t_seq_lens,
-                            bt.t_q_start, max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len,
-                            sliding_window=l.window, sinks=l.sinks, out=outs[li], workspace=ws[li])
-
-    def step():
-        for li in range(len(bt.layers)):
-            attention(li)
-        av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start, argmax_out=am, accept_len=acc,
-                         num_emitted=ne, emitted=em, workspace=aws)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    run_step = step
-    if args.graph:
-        # The step's launches, captured once: a serving loop replays them
-        # without per-kernel launch work on the host.
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step()
-        graph.replay()
-        torch.cuda.synchronize()
-        run_step = graph.replay
-
-    # timed region: K whole steps, no events inside
     K = args.steps
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t0.record(stream)
-    for k in range(K):
-        run_step()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_step = t0.elapsed_time(t1) / K
-
-    # average duration of one attention call (roofline): K calls of the layer
-    # launched back to back on the launch stream, HIP events at the two ends of
-    # that region, after the timed steps
-    attn_ms = []
-    for li in range(len(bt.layers)):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    per_seed = []
+    first = None   # the first seed's batch and buffers, kept for the side measurements
+    for seed in seeds:
+        log("config", cfg.name, "seed", seed)
+        bt = workload.make_batch(cfg, seed, dev)
         torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(K):
-            attention(li)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        attn_ms.append(e0.elapsed_time(e1) / K)
+        outs = [torch.empty_like(l.q) for l in bt.layers]
+        ws = []
+        for l in bt.layers:
+            nb = av.attention_workspace_size(l.q, l.k_cache, bt.t_block_tables, max_q_len=bt.max_q_len,
+                                             max_seq_len=bt.max_seq_len, sliding_window=l.window)
+            ws.append(torch.empty(max(nb, 1), dtype=torch.uint8, device=dev))
+        T, B = bt.total_q, len(bt.seq_lens)
+        acc = torch.empty(B, dtype=torch.int32, device=dev)
+        ne = torch.empty(B, dtype=torch.int32, device=dev)
+        em = torch.empty(T, dtype=torch.int32, device=dev)
+        am = torch.empty(T, dtype=torch.int32, device=dev)
+        aws = torch.empty(max(1, av.accept_workspace_size(B, T, cfg.vocab, code)), dtype=torch.uint8,
+                          device=dev)
 
-    emitted = int(ne.sum().item())
-    proposed = int(bt.num_drafts.sum())
-    accepted = int(acc.sum().item())
-    value = emitted / (ms_step * 1e-3)
-    # dominant kernel: the attention layer with the most algorithmic bytes
-    abytes = [attention_bytes(bt, l) for l in bt.layers]
-    dom = int(np.argmax(abytes))
-    achieved = abytes[dom] / (attn_ms[dom] * 1e-3) / 1e9
-    step_bytes = sum(abytes) + accept_bytes(bt)
-    log("step %.3f ms (wall %.3f ms); attention calls timed alone %s ms" % (
-        ms_step, wall / K * 1e3, ["%.3f" % x for x in attn_ms]))
-    log("step algorithmic bytes %.3f GB -> %.0f GB/s (%.1f%% of HBM peak); attention layer %d: "
-        "%.3f GB in %.3f ms = %.0f GB/s" % (step_bytes / 1e9, step_bytes / ms_step / 1e6,
-                                            100 * step_bytes / ms_step / 1e6 / HBM_PEAK_GBS, dom,
-                                            abytes[dom] / 1e9, attn_ms[dom], achieved))
-    log("drafts proposed %d accepted %d (rejection rate %.3f), emitted %d, scored positions %d" % (
-        proposed, accepted, 1 - accepted / max(1, proposed), emitted, T))
+        def attention(li, bt=bt, outs=outs, ws=ws):
+            l = bt.layers[li]
+            av.verify_attention(l.q, l.k_cache, l.v_cache, bt.t_block_tables, bt.t_seq_lens,
+                                bt.t_q_start, max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len,
+                                sliding_window=l.window, sinks=l.sinks, out=outs[li], workspace=ws[li])
+
+        def step(bt=bt, acc=acc, ne=ne, em=em, am=am, aws=aws, attention=attention):
+            for li in range(len(bt.layers)):
+                attention(li)
+            av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start, argmax_out=am, accept_len=acc,
+                             num_emitted=ne, emitted=em, workspace=aws)
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        run_step = step
+        if args.graph:
+            # The step's launches, captured once: a serving loop replays them
+            # without per-kernel launch work on the host.
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                step()
+            graph.replay()
+            torch.cuda.synchronize()
+            run_step = graph.replay
+
+        # timed region: K whole steps back to back, one HIP event between
+        # consecutive steps (no other synchronisation inside)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        evs[0].record(stream)
+        for k in range(K):
+            run_step()
+            evs[k + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        step_ms = [evs[k].elapsed_time(evs[k + 1]) for k in range(K)]
+        med_ms = statistics.median(step_ms)
+        mean_ms = evs[0].elapsed_time(evs[K]) / K
+        # the same K steps with events only at the two ends (what an event
+        # between steps costs shows as the difference to mean_ms)
+        torch.cuda.synchronize()
+        evs[0].record(stream)
+        for k in range(K):
+            run_step()
+        evs[1].record(stream)
+        torch.cuda.synchronize()
+        plain_ms = evs[0].elapsed_time(evs[1]) / K
+
+        # average duration of one attention call (roofline): K calls of the
+        # layer launched back to back on the launch stream, HIP events at the
+        # two ends of that region, after the timed steps
+        attn_ms = []
+        for li in range(len(bt.layers)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(K):
+                attention(li)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            attn_ms.append(e0.elapsed_time(e1) / K)
+
+        emitted = int(ne.sum().item())
+        proposed = int(bt.num_drafts.sum())
+        accepted = int(acc.sum().item())
+        abytes = [attention_bytes(bt, l) for l in bt.layers]
+        dom = int(np.argmax(abytes))
+        step_bytes = sum(abytes) + accept_bytes(bt)
+        r = dict(seed=seed, median_ms=med_ms, mean_ms=mean_ms, plain_ms=plain_ms, min_ms=min(step_ms),
+                 max_ms=max(step_ms), wall_ms=wall / K * 1e3, emitted=emitted, proposed=proposed,
+                 accepted=accepted, T=T, value=emitted / (med_ms * 1e-3), attn_ms=attn_ms,
+                 abytes=abytes, dom=dom, achieved=abytes[dom] / (attn_ms[dom] * 1e-3) / 1e9,
+                 step_bytes=step_bytes, mean_context=float(bt.context_len.mean()))
+        per_seed.append(r)
+        log("seed %d: step median %.4f ms (mean %.4f, without inner events %.4f, min %.4f, max %.4f; "
+            "wall %.4f); attention "
+            "calls timed alone %s ms; emitted %d -> %.0f verified tok/s; attention layer %d %.3f GB "
+            "-> %.0f GB/s" % (seed, med_ms, mean_ms, plain_ms, r["min_ms"], r["max_ms"], r["wall_ms"],
+                              ["%.4f" % x for x in attn_ms], emitted, r["value"], dom,
+                              abytes[dom] / 1e9, r["achieved"]))
+        if first is None:
+            first = dict(bt=bt, aws=aws, abytes=abytes, dom=dom)
+        else:
+            del bt, outs, ws, aws, step, attention, run_step
+            torch.cuda.empty_cache()
+
+    bt, aws, abytes, dom = first["bt"], first["aws"], first["abytes"], first["dom"]
+    T, B = bt.total_q, len(bt.seq_lens)
+    mean = lambda k: float(np.mean([r[k] for r in per_seed]))
+    value = mean("value")
+    ms_step = mean("median_ms")
+    achieved = mean("achieved")
+    step_frac = float(np.mean([r["step_bytes"] / r["median_ms"] / 1e6 / HBM_PEAK_GBS for r in per_seed]))
+    proposed, accepted = sum(r["proposed"] for r in per_seed), sum(r["accepted"] for r in per_seed)
+    log("over %d seed(s): %.0f verified tok/s (mean of per-seed medians), step %.4f ms, attention "
+        "%.0f GB/s (%.3f of peak), step %.3f of peak; drafts proposed %d accepted %d" % (
+            len(seeds), value, ms_step, achieved, achieved / HBM_PEAK_GBS, step_frac, proposed,
+            accepted))
 
     if args.copy_calibration:
         x = torch.zeros(CALIB_BYTES // 4, dtype=torch.int32, device=dev)
@@ -474,18 +711,22 @@ def main():
         torch.cuda.synchronize()
         del x, y
 
-    budget = budget_timing(av, workload, oracle_ok=args.cpu_budget > 0, batch=B, steps=K, dev=dev)
-    log("budget allocation (verify_budget):", budget)
-    append = kv_append_timing(av, bt, K)
-    log("KV append (verify_kv_append):", append)
-    accept_t = accept_timing(av, bt, K, aws)
-    log("acceptance calls:", accept_t)
-    lmhead = lmhead_timing(av, workload, bt, K) if cfg.dtype == "bf16" else None
-    log("LM head fused with acceptance (verify_lmhead_accept):", lmhead)
+    ceil = budget = append = accept_t = lmhead = None
+    if args.side:
+        ceil = ceilings(bt, bt.layers[dom])
+        log("same-run ceilings:", ceil)
+        budget = budget_timing(av, workload, oracle_ok=args.cpu_budget > 0, batch=B, steps=K, dev=dev)
+        log("budget allocation (verify_budget):", budget)
+        append = kv_append_timing(av, bt, K)
+        log("KV append (verify_kv_append):", append)
+        accept_t = accept_timing(av, bt, K, aws)
+        log("acceptance calls:", accept_t)
+        lmhead = lmhead_timing(av, workload, bt, K) if cfg.dtype == "bf16" else None
+        log("LM head fused with acceptance (verify_lmhead_accept):", lmhead)
 
     traffic = stored_traffic(cfg.name)
     if traffic is not None:
-        log("HBM traffic per attention call (counters): %.4f GB vs algorithmic %.4f GB" % (
+        log("HBM traffic per attention call (counters, seed 0): %.4f GB vs algorithmic %.4f GB" % (
             traffic / 1e9, abytes[dom] / 1e9))
 
     cpu = None
@@ -494,6 +735,16 @@ def main():
         cpu = cpu_baseline(bt, args.cpu_budget)
         log("cpu baseline", cpu)
 
+    roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+            "algorithmic_bytes": mean("abytes") if len(bt.layers) == 1 else abytes[dom],
+            "kernel": "verify_attention call (attn_persist + attn_combine_slots), layer %d" % dom}
+    if ceil:
+        roof.update(ceiling_GBps=ceil["gather_GBps"], ceiling_frac=achieved / ceil["gather_GBps"],
+                    ceiling_kind="torch index_select of the call's K/V tiles through the block "
+                                 "table, bytes read + written",
+                    copy_ceiling_GBps=ceil["copy_GBps"],
+                    copy_ceiling_frac=achieved / ceil["copy_GBps"])
     res = {
         "metric": "verified tokens/sec per verify step (1 GPU) + achieved HBM GB/s vs peak",
         "value": value,
@@ -508,18 +759,17 @@ def main():
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": cfg.name, "description": cfg.description, "batch": B,
-                   "total_q": T, "mean_context": float(bt.context_len.mean()),
+                   "total_q": T, "mean_context": mean("mean_context"),
                    "num_q_heads": cfg.num_q_heads, "num_kv_heads": cfg.num_kv_heads,
                    "head_dim": cfg.head_dim, "vocab": cfg.vocab, "layers": len(bt.layers),
-                   "seed": args.seed, "hip_graph": bool(args.graph)},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "algorithmic_bytes": abytes[dom],
-                     "kernel": "verify_attention call (attn_persist + attn_combine_slots), "
-                               "layer %d" % dom},
-        "step_hbm_frac": step_bytes / ms_step / 1e6 / HBM_PEAK_GBS,
-        "scored_positions_per_s": T / (ms_step * 1e-3),
+                   "seeds": seeds, "hip_graph": bool(args.graph)},
+        "roofline": roof,
+        "step_hbm_frac": step_frac,
+        "scored_positions_per_s": float(np.mean([r["T"] / (r["median_ms"] * 1e-3) for r in per_seed])),
         "rejection_rate": 1 - accepted / max(1, proposed),
+        "per_seed": [{k: r[k] for k in ("seed", "median_ms", "mean_ms", "plain_ms", "min_ms", "max_ms",
+                                        "emitted",
+                                        "value", "achieved")} for r in per_seed],
         "cpu_baseline": cpu,
         "budget_alloc": budget,
         "kv_append": append,

@@ -27,6 +27,11 @@ HIPCC_FLAGS = [
     "-Wall",
     # keep the compiler from emitting packed fp32 arithmetic (v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in ordinary VGPRs: the attention kernels rescale their
+    # output accumulators with VALU arithmetic every block, and with the
+    # accumulators in AGPRs the compiler copied all of them to VGPRs and back
+    # around every block (about 200 extra VALU instructions per KV block)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 
