@@ -138,6 +138,25 @@ int verify_attention(const verify_attn_params *params, int32_t total_q, int32_t 
                      void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * verify_attention_plan -- the work decomposition verify_attention would use
+ * for the same arguments, for tests and tools (nothing is launched).
+ *
+ *   info[0]  1: bf16 persistent MFMA schedule, 0: fp32 split-K VALU kernel
+ *   bf16:    info[1] workgroups sharing the units, info[2] query rows per row
+ *            group, info[3] row groups per (request, KV head) at most,
+ *            info[4] fixed units per workgroup (0: equal shares).  A unit is
+ *            one 16-token block of one (request, KV head, row group) pair;
+ *            units are numbered request by request, then KV head, then row
+ *            group, then block, and workgroup w owns units
+ *            [U w / N, U (w + 1) / N) of the U units (N = min(info[1], U)).
+ *   fp32:    info[1] splits per request at most, info[2] query rows per work
+ *            item, info[3] row groups, info[4] KV blocks per split.
+ * Same argument checks as verify_attention_workspace_size.
+ */
+int verify_attention_plan(const verify_attn_params *params, int32_t total_q, int32_t max_q_len,
+                          int32_t max_seq_len, int32_t *info);
+
+/*
  * verify_kv_append -- the verify step's new tokens' K and V into the paged
  * cache (the K/V that verify_attention reads for positions S_i - n_i .. S_i - 1).
  *

@@ -21,7 +21,8 @@ from .build import LIB_PATH
 
 __all__ = ["verify_attention", "verify_accept", "verify_accept_noalloc", "verify_accept_sampled",
            "verify_lmhead_accept",
-           "verify_budget", "verify_kv_append", "attention_workspace_size", "accept_workspace_size",
+           "verify_budget", "verify_kv_append", "attention_workspace_size", "attention_plan",
+           "accept_workspace_size",
            "lmhead_accept_workspace_size", "VerifyError", "library", "abi_version", "F32", "BF16"]
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
@@ -70,6 +71,8 @@ def library(path: Optional[str] = None):
     lib.verify_attention_workspace_size.restype = ctypes.c_int
     lib.verify_attention.argtypes = [P, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.verify_attention.restype = ctypes.c_int
+    lib.verify_attention_plan.argtypes = [P, i32, i32, i32, ctypes.POINTER(i32)]
+    lib.verify_attention_plan.restype = ctypes.c_int
     lib.verify_kv_append.argtypes = [P, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.verify_kv_append.restype = ctypes.c_int
     lib.verify_accept_workspace_size.argtypes = [i32, i32, i64, i32, ctypes.POINTER(sz)]
@@ -214,6 +217,18 @@ def attention_workspace_size(q, k_cache, block_tables, *, max_q_len: int, max_se
                                                      int(max_seq_len), ctypes.byref(n)),
            "verify_attention_workspace_size")
     return int(n.value)
+
+
+def attention_plan(q, k_cache, block_tables, *, max_q_len: int, max_seq_len: int,
+                   sliding_window: int = 0, scale: float = 0.0, kv_split_blocks: int = 0) -> dict:
+    """The work decomposition verify_attention would use (nothing is launched)."""
+    p = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
+    info = (ctypes.c_int32 * 5)()
+    _check(library().verify_attention_plan(ctypes.byref(p), int(q.shape[0]), int(max_q_len),
+                                           int(max_seq_len), info), "verify_attention_plan")
+    keys = (("mfma", "workgroups", "rows_per_group", "row_groups", "units_per_workgroup") if info[0]
+            else ("mfma", "splits", "rows_per_item", "row_groups", "split_blocks"))
+    return dict(zip(keys, [int(x) for x in info]))
 
 
 def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, max_q_len: int,

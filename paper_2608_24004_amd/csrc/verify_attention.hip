@@ -1299,6 +1299,30 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
     return check_launch();
 }
 
+extern "C" int verify_attention_plan(const verify_attn_params* params, int32_t total_q,
+                                     int32_t max_q_len, int32_t max_seq_len, int32_t* info) {
+    if (!info) return VERIFY_EINVAL;
+    int rc = validate(params, total_q, max_q_len, max_seq_len);
+    if (rc != VERIFY_OK) return rc;
+    AttnPlan pl;
+    rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl);
+    if (rc != VERIFY_OK) return rc;
+    if (pl.mfma) {
+        info[0] = 1;
+        info[1] = pl.nwg;
+        info[2] = pl.nw * pl.tpw * 16;
+        info[3] = pl.rg_max;
+        info[4] = pl.spb;
+    } else {
+        info[0] = 0;
+        info[1] = pl.max_splits;
+        info[2] = kValuRows;
+        info[3] = pl.row_groups;
+        info[4] = pl.split_blocks;
+    }
+    return VERIFY_OK;
+}
+
 extern "C" int verify_kv_append(const verify_attn_params* params, int32_t total_q,
                                 const void* k_new, const void* v_new, const int32_t* block_tables,
                                 const int32_t* seq_lens, const int32_t* q_start, void* k_cache,

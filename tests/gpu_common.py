@@ -95,3 +95,43 @@ def oracle_accept_all(logits, q_start, tokens, dtype_code):
     am, gap = oracle.argmax(workload.host_storage(logits), dtype_code)
     acc, ne, em = oracle.accept(q_start, tokens, am)
     return am, gap, acc, ne, em
+
+
+def pair_schedule(batch, layer, plan):
+    """(request, KV head, row group) pairs of the persistent bf16 schedule and
+    whether a workgroup range boundary cuts each one (its first and last KV
+    blocks belong to different workgroups), from the plan verify_attention
+    reports: the unit numbering and the equal-share ranges it documents."""
+    cfg = batch.cfg
+    G = cfg.num_q_heads // cfg.num_kv_heads
+    rpg, rg_max, nwg = plan["rows_per_group"], plan["row_groups"], plan["workgroups"]
+    n = np.diff(batch.q_start).astype(np.int64)
+    S = batch.seq_lens.astype(np.int64)
+    W = layer.window
+    key_lo = np.maximum(0, S - n - W + 1) if W > 0 else np.zeros_like(S)
+    nb = np.maximum(0, (S + 15) // 16 - key_lo // 16)
+    rg = np.minimum(rg_max, (G * n + rpg - 1) // rpg)
+    units = cfg.num_kv_heads * rg * nb
+    start = np.concatenate([[0], np.cumsum(units)])
+    U = int(start[-1])
+    N = min(nwg, max(U, 1))
+    owner = lambda u: ((u + 1) * N - 1) // max(U, 1)
+    pairs = []
+    for i in range(len(n)):
+        for g in range(cfg.num_kv_heads):
+            for r in range(int(rg[i])):
+                if nb[i] == 0:
+                    continue
+                ps = int(start[i]) + (g * int(rg[i]) + r) * int(nb[i])
+                pairs.append((i, g, r, owner(ps) != owner(ps + int(nb[i]) - 1)))
+    return pairs
+
+
+def pair_vectors(batch, pair, rows_per_group):
+    """(rows, heads) of the output vectors a pair computes."""
+    i, g, r, _ = pair
+    cfg = batch.cfg
+    G = cfg.num_q_heads // cfg.num_kv_heads
+    q0, q1 = int(batch.q_start[i]), int(batch.q_start[i + 1])
+    local = np.arange(r * rows_per_group, min((r + 1) * rows_per_group, G * (q1 - q0)))
+    return (q0 + local // G).astype(np.int32), (g * G + local % G).astype(np.int32)

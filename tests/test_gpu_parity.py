@@ -17,7 +17,7 @@ import oracle
 import paper_2608_24004_amd as av
 import workload
 from gpu_common import (NEAR_TIE, assert_attention_close, compact_for_rows, gpu_attention,
-                        oracle_accept_all, sample_pairs, to_host_f64)
+                        oracle_accept_all, pair_schedule, to_host_f64)
 from helpers import Paged, random_paged
 
 pytestmark = pytest.mark.gpu
@@ -31,11 +31,12 @@ def say(*a):
 # --------------------------------------------------------------------------- accept
 
 
+@pytest.mark.parametrize("seed", range(5))
 @pytest.mark.parametrize("name", list(workload.CONFIGS))
-def test_accept_full_size(name):
+def test_accept_full_size(name, seed):
     cfg = workload.CONFIGS[name]
-    say("accept full", name)
-    bt = workload.make_batch(cfg, 0, DEV, with_layers=False)
+    say("accept full", name, "seed", seed)
+    bt = workload.make_batch(cfg, seed, DEV, with_layers=False)
     acc, ne, em, am = av.verify_accept(bt.logits, bt.t_tokens, bt.t_q_start)
     torch.cuda.synchronize()
     r_am, gap, r_acc, r_ne, r_em = oracle_accept_all(bt.logits, bt.q_start, bt.tokens,
@@ -271,22 +272,86 @@ def test_attention_long_pairs(hq, hkv, d):
         _check_paged(p, split=split, what="long pairs split=%d" % split)
 
 
-@pytest.mark.parametrize("name", list(workload.CONFIGS))
-def test_attention_full_size_sampled(name):
-    cfg = workload.CONFIGS[name]
-    say("attn full", name)
-    bt = workload.make_batch(cfg, 0, DEV, with_logits=False)
-    rows, heads = sample_pairs(bt, 160, seed=1)
+SEEDS = range(5)
+EVERY_PAIR = ["qwen3_8b", "dsk_distill_8b", "gpt_oss_20b"]
+
+
+def _attention_layers(bt):
     for layer in bt.layers:
         out = gpu_attention(layer.q, layer.k_cache, layer.v_cache, bt.t_block_tables,
                             bt.t_seq_lens, bt.t_q_start, max_q_len=bt.max_q_len,
                             max_seq_len=bt.max_seq_len, window=layer.window, sinks=layer.sinks)
+        plan = av.attention_plan(layer.q, layer.k_cache, bt.t_block_tables, max_q_len=bt.max_q_len,
+                                 max_seq_len=bt.max_seq_len, sliding_window=layer.window)
+        yield layer, out, plan
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+@pytest.mark.parametrize("name", EVERY_PAIR)
+def test_attention_full_size_every_vector(name, seed):
+    """Every (row, head) output vector of every layer at full size, in the
+    launch configuration bench.py times, for five seeds; the pairs that
+    workgroup range boundaries cut (merged by attn_combine_slots) are among
+    them, and their count is asserted."""
+    cfg = workload.CONFIGS[name]
+    say("attn full every vector", name, "seed", seed)
+    bt = workload.make_batch(cfg, seed, DEV, with_logits=False)
+    code = workload.dtype_code(cfg.dtype)
+    for layer, out, plan in _attention_layers(bt):
+        got = to_host_f64(out)
+        ref = oracle.attention(num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
+                               head_dim=cfg.head_dim, sliding_window=layer.window, scale=0.0,
+                               dtype=code, q=workload.host_storage(layer.q),
+                               k_cache=workload.host_storage(layer.k_cache),
+                               v_cache=workload.host_storage(layer.v_cache),
+                               block_tables=bt.block_tables, seq_lens=bt.seq_lens,
+                               q_start=bt.q_start,
+                               sinks=None if layer.sinks is None else layer.sinks.cpu().numpy())
+        err = assert_attention_close(got, ref, cfg.dtype, "%s seed %d window=%d" % (
+            name, seed, layer.window))
+        pairs = pair_schedule(bt, layer, plan)
+        cut = sum(p[3] for p in pairs)
+        say("  window", layer.window, "vectors", got.shape[0] * got.shape[1], "max rel err", err,
+            "pairs", len(pairs), "cut", cut, "plan", plan)
+        assert cut > 0
+        del out
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_attention_long_context_sampled(seed):
+    """The long-context stress at full size (43 GB of KV): every (row, head)
+    of sampled requests -- the fewest and most drafts, the longest context,
+    and a request with a pair cut by a workgroup range boundary -- plus random
+    extra vectors."""
+    name = "long_context"
+    cfg = workload.CONFIGS[name]
+    say("attn long context", "seed", seed)
+    bt = workload.make_batch(cfg, seed, DEV, with_logits=False)
+    for layer, out, plan in _attention_layers(bt):
+        pairs = pair_schedule(bt, layer, plan)
+        cut_reqs = sorted({p[0] for p in pairs if p[3]})
+        assert cut_reqs
+        n = np.diff(bt.q_start)
+        want = {int(np.argmin(n)), int(np.argmax(n)), int(np.argmax(bt.seq_lens)),
+                cut_reqs[seed % len(cut_reqs)]}
+        rng = np.random.default_rng(seed)
+        others = [i for i in rng.permutation(len(n)) if i not in want]
+        reqs = sorted(want | set(others[:2]))
+        Hq = cfg.num_q_heads
+        rows = np.concatenate([np.repeat(np.arange(bt.q_start[i], bt.q_start[i + 1]), Hq)
+                               for i in reqs]).astype(np.int32)
+        heads = np.concatenate([np.tile(np.arange(Hq), int(n[i])) for i in reqs]).astype(np.int32)
+        extra = rng.integers(0, bt.total_q, size=64).astype(np.int32)
+        xh = rng.integers(0, Hq, size=64).astype(np.int32)
+        rows, heads = np.concatenate([rows, extra]), np.concatenate([heads, xh])
         got = to_host_f64(out[torch.as_tensor(rows, device=DEV, dtype=torch.int64),
                               torch.as_tensor(heads, device=DEV, dtype=torch.int64)])
         args, rows_c = compact_for_rows(bt, layer, rows)
         ref = oracle.attention(rows=rows_c, heads=heads, **args)
-        err = assert_attention_close(got, ref, cfg.dtype, "%s window=%d" % (name, layer.window))
-        say("  window", layer.window, "max rel err", err)
+        err = assert_attention_close(got, ref, cfg.dtype, "%s seed %d" % (name, seed))
+        say("  requests", reqs, "cut-pair requests", len(cut_reqs), "vectors", rows.size,
+            "max rel err", err)
         assert torch.isfinite(out.float()).all()
         del out
     torch.cuda.empty_cache()

@@ -60,11 +60,12 @@ def _plant(y, q_start, rng, vocab):
     return tokens
 
 
-@pytest.mark.parametrize("name", list(workload.CONFIGS))
-def test_sampled_full_size(name):
+@pytest.mark.parametrize("name,seed", [(n, s) for n in workload.CONFIGS for s in range(5)
+                                        if n != "long_context" or s < 2])
+def test_sampled_full_size(name, seed):
     cfg = workload.CONFIGS[name]
-    say("sampled full", name)
-    bt = workload.make_batch(cfg, 0, DEV, with_layers=False)
+    say("sampled full", name, "seed", seed)
+    bt = workload.make_batch(cfg, seed, DEV, with_layers=False)
     code = workload.dtype_code(cfg.dtype)
     T, seed, offset = 0.7, 0x1234_5678_9ABC_DEF0, 11
     y_ref = oracle.sample(workload.host_storage(bt.logits), code, T, seed=seed, offset=offset)
