@@ -122,7 +122,11 @@ typedef struct verify_attn_params {
  *   out          [total_q][Hq][D]                     (dtype); a row with no
  *                visible key (S_i < n_i) is written as zeros
  *   max_q_len    host upper bound on n_i; max_seq_len host upper bound on S_i
- *                (they size the launch; tighter bounds launch less idle work)
+ *                (they size the launch; tighter bounds launch less idle work).
+ *                Rows of a request with n_i > max_q_len that the launch does
+ *                not reach (verify_attention_plan gives the reach: rows j with
+ *                j * (Hq/Hkv) + h % (Hq/Hkv) below info[3] * info[2]) are not
+ *                computed: their outputs are written as quiet NaN.
  *   workspace    device scratch of at least the size returned by
  *                verify_attention_workspace_size() for the same (params,
  *                total_q, max_q_len, max_seq_len); may be NULL if that size is

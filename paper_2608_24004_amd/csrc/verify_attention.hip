@@ -358,6 +358,25 @@ __device__ __forceinline__ ReqGeom req_geom(const PArgs& a, const int32_t* __res
     return r;
 }
 
+// Rows past the launch's reach: a request with more than max_q_len rows can
+// need more row groups than the launch provides (rg_max); those rows are not
+// computed, and their outputs are written as a quiet NaN instead of being
+// left stale.  Threads t = t0, t0 + nt, ... cover the batch's requests.
+template <int D>
+__device__ void mark_unreached_rows(const PArgs& a, const int32_t* __restrict__ q_start,
+                                    uint16_t* __restrict__ out, int t0, int nt) {
+    const int reach = a.rg_max * a.rows_per_group;  // local rows of one (request, KV head)
+    for (int i = t0; i < a.num_seqs; i += nt) {
+        const int q0 = q_start[i];
+        const int rows = a.group * (q_start[i + 1] - q0);
+        for (int rr = reach; rr < rows; ++rr)
+            for (int g = 0; g < a.hkv; ++g) {
+                const int64_t hrow = (int64_t)(q0 + rr / a.group) * a.hq + g * a.group + rr % a.group;
+                for (int d = 0; d < D; ++d) out[hrow * D + d] = 0x7fc0;  // bf16 quiet NaN
+            }
+    }
+}
+
 // Workgroups that share the U units in equal-share mode: at most one per unit,
 // so that every participating workgroup owns at least one unit.
 __device__ __forceinline__ int sharing_wgs(const PArgs& a, int U) { return min(a.nwg, max(U, 1)); }
@@ -369,9 +388,12 @@ __device__ __forceinline__ int owner_of(const PArgs& a, int u, int U) {
 }
 
 // One workgroup: exclusive prefix sum of Hkv * row_groups * blocks over the batch.
+template <int D>
 __global__ __launch_bounds__(1024) void attn_schedule(PArgs a, const int32_t* __restrict__ q_start,
                                                      const int32_t* __restrict__ seq_lens,
-                                                     int32_t* __restrict__ unit_start) {
+                                                     int32_t* __restrict__ unit_start,
+                                                     uint16_t* __restrict__ out) {
+    mark_unreached_rows<D>(a, q_start, out, threadIdx.x, blockDim.x);
     __shared__ int wsum[16];
     __shared__ int carry_s;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
@@ -595,8 +617,10 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     if (a.inline_sched) {
         if (wv == 0) {
             sched_prefix(a, q_start, seq_lens, sched, lane);
-            if (w == 0)
+            if (w == 0) {
                 for (int i = lane; i <= a.num_seqs; i += kWave) unit_start[i] = sched[i];
+                mark_unreached_rows<D>(a, q_start, out, lane, kWave);
+            }
         }
         __syncthreads();
         ustart = sched;
@@ -906,8 +930,19 @@ __global__ __launch_bounds__(kAttnThreads) void attn_combine(AttnArgs a, int tot
         if (a.q_start[mid] <= row) lo = mid; else hi = mid - 1;
     }
     const SeqGeom sg = seq_geom(a, lo);
-    if (sg.nsplit == 1) return;
     T* outp = static_cast<T*>(a.out);
+    {
+        // rows past the launch's reach (a request with more than max_q_len
+        // rows) are not computed: quiet NaN instead of stale memory
+        const int h = (int)(item - (int64_t)row * a.hq);
+        const int rr = (row - sg.q0) * a.group + h % a.group;
+        if (rr >= a.row_groups * kValuRows) {
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) Storage<T>::store(outp, item * D + lane * DPL + e, __builtin_nanf(""));
+            return;
+        }
+    }
+    if (sg.nsplit == 1) return;
     float acc[DPL];
 #pragma unroll
     for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
@@ -940,32 +975,52 @@ __global__ __launch_bounds__(kAttnThreads) void attn_combine(AttnArgs a, int tot
 // The verify step's new tokens (row j of request i sits at position
 // p = S_i - n_i + j) get their K and V written into slot p % 16 of block
 // block_tables[i][p / 16]: K x-packed ([D/x][16][x] per block and head), V
-// transposed ([D][16]).  One workgroup per (row, KV head); thread d moves
-// dimension d.  Rows with a negative position or a block id outside
-// [0, num_blocks) are skipped.
+// transposed ([D][16]).  One workgroup per (request, KV head) writes all of
+// the request's new tokens of that head, so the tokens that share a 32-byte
+// V sector (consecutive slots of one dimension) are written by one compute
+// unit and leave its L2 as one sector.  K moves in 16-byte chunks, thread
+// items ordered (chunk, token) so that consecutive threads write consecutive
+// slots; V moves element by element, items ordered (dimension, token).
+// Tokens with a negative position or a block id outside [0, num_blocks) are
+// skipped.
+constexpr int kAppendThreads = 256;
+
 template <typename T, int D>
-__global__ __launch_bounds__(D) void attn_kv_append(
+__global__ __launch_bounds__(kAppendThreads) void attn_kv_append(
     int num_seqs, int hkv, int max_blocks, int num_blocks, const T* __restrict__ k_new,
     const T* __restrict__ v_new, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start, T* __restrict__ kc,
     T* __restrict__ vc) {
     constexpr int X = Storage<T>::kPer16B;
-    const int row = blockIdx.x, g = blockIdx.y, d = threadIdx.x;
-    int lo = 0, hi = num_seqs - 1;  // request owning the row: largest i with q_start[i] <= row
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (q_start[mid] <= row) lo = mid; else hi = mid - 1;
+    constexpr int NC = D / X;  // 16-byte chunks per key
+    const int i = blockIdx.x, g = blockIdx.y;
+    const int q0 = q_start[i];
+    const int n = q_start[i + 1] - q0;
+    if (n <= 0) return;
+    const int64_t p0 = (int64_t)seq_lens[i] - n;  // position of the request's row 0
+    const int32_t* bt = block_tables + (int64_t)i * max_blocks;
+    // physical block of token j, or -1 when the token is skipped
+    auto block_of = [&](int j) {
+        const int64_t p = p0 + j;
+        if (p < 0 || p / kBlockTokens >= max_blocks) return -1;
+        const int b = bt[p / kBlockTokens];
+        return (b < 0 || b >= num_blocks) ? -1 : b;
+    };
+    for (int it = threadIdx.x; it < n * NC; it += kAppendThreads) {
+        const int c = it / n, j = it - c * n;
+        const int b = block_of(j);
+        if (b < 0) continue;
+        const int t = (int)((p0 + j) % kBlockTokens);
+        const uint4 v = ld16(k_new + ((int64_t)(q0 + j) * hkv + g) * D + c * X);
+        *reinterpret_cast<uint4*>(kc + ((((int64_t)b * hkv + g) * NC + c) * kBlockTokens + t) * X) = v;
     }
-    const int n = q_start[lo + 1] - q_start[lo];
-    const int64_t p = (int64_t)seq_lens[lo] - n + (row - q_start[lo]);
-    if (p < 0 || p / kBlockTokens >= max_blocks) return;
-    const int b = block_tables[(int64_t)lo * max_blocks + p / kBlockTokens];
-    if (b < 0 || b >= num_blocks) return;
-    const int t = (int)(p % kBlockTokens);
-    const int64_t src = ((int64_t)row * hkv + g) * D + d;
-    const int64_t bh = (int64_t)b * hkv + g;
-    kc[((bh * (D / X) + d / X) * kBlockTokens + t) * X + d % X] = k_new[src];
-    vc[(bh * D + d) * kBlockTokens + t] = v_new[src];
+    for (int it = threadIdx.x; it < n * D; it += kAppendThreads) {
+        const int d = it / n, j = it - d * n;
+        const int b = block_of(j);
+        if (b < 0) continue;
+        const int t = (int)((p0 + j) % kBlockTokens);
+        vc[(((int64_t)b * hkv + g) * D + d) * kBlockTokens + t] = v_new[((int64_t)(q0 + j) * hkv + g) * D + d];
+    }
 }
 
 // ------------------------------------------------------------------ host side
@@ -1163,11 +1218,11 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
 // merge of partial slots.  Returns false if the plan names no known shape.
 bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, int head_dim,
                     int max_rows, hipStream_t stream) {
-    if (!a.inline_sched)
-        hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a, m.q_start, m.seq_lens,
-                           m.unit_start);
     return with_shape(head_dim, pl.nw, pl.tpw, [&](auto sh) {
         using S = decltype(sh);
+        if (!a.inline_sched)
+            hipLaunchKernelGGL((attn_schedule<S::D>), dim3(1), dim3(1024), 0, stream, a, m.q_start,
+                               m.seq_lens, m.unit_start, m.out);
         hipLaunchKernelGGL(persist_kernel<S>(), dim3(a.nwg), dim3(S::NW * kWave), 0, stream, a, m.q,
                            m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start, m.unit_start, m.out,
                            m.slot_o, m.slot_lse);
@@ -1334,9 +1389,10 @@ extern "C" int verify_kv_append(const verify_attn_params* params, int32_t total_
     if (!k_new || !v_new || !block_tables || !seq_lens || !q_start || !k_cache || !v_cache)
         return VERIFY_EINVAL;
     if (p.num_kv_heads > 65535) return VERIFY_EUNSUPPORTED;  // grid y
-    const dim3 grid((unsigned)total_q, (unsigned)p.num_kv_heads);
+    const dim3 grid((unsigned)p.num_seqs, (unsigned)p.num_kv_heads);
 #define AVERIFY_APPEND(T, D)                                                                       \
-    hipLaunchKernelGGL((attn_kv_append<T, D>), grid, dim3(D), 0, stream, p.num_seqs, p.num_kv_heads, \
+    hipLaunchKernelGGL((attn_kv_append<T, D>), grid, dim3(kAppendThreads), 0, stream, p.num_seqs,    \
+                       p.num_kv_heads,                                                             \
                        p.max_blocks_per_seq, p.num_blocks, static_cast<const T*>(k_new),          \
                        static_cast<const T*>(v_new), block_tables, seq_lens, q_start,             \
                        static_cast<T*>(k_cache), static_cast<T*>(v_cache))

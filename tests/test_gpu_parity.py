@@ -161,6 +161,35 @@ SHAPES = [(8, 2, 64), (32, 8, 128), (64, 8, 64), (4, 4, 128), (8, 1, 128), (16, 
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("hq,hkv,d", [(8, 2, 64), (32, 8, 128)])
+@pytest.mark.parametrize("split", [0, 2])
+def test_attention_rows_past_max_q_len(dtype, hq, hkv, d, split):
+    """max_q_len below a request's row count: the rows the launch reaches
+    (computed on the host from the plan) match the oracle, the rest are NaN."""
+    say("attn max_q_len too small", dtype, hq, hkv, d, split)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                     contexts=[40, 300, 5, 77], drafts=[8, 2, 16, 0], seed=hq + d)
+    dv = _to_dev(p)
+    max_q_len = 3
+    out = gpu_attention(dv["q"], dv["kc"], dv["vc"], dv["bt"], dv["sl"], dv["qs"],
+                        max_q_len=max_q_len, max_seq_len=int(p.seq_lens.max()), split=split)
+    plan = av.attention_plan(dv["q"], dv["kc"], dv["bt"], max_q_len=max_q_len,
+                             max_seq_len=int(p.seq_lens.max()), kv_split_blocks=split)
+    reach = plan["row_groups"] * (plan["rows_per_group"] if plan["mfma"] else plan["rows_per_item"])
+    got = to_host_f64(out)
+    ref = oracle.attention(**p.oracle_args())
+    G = hq // hkv
+    reached = np.zeros((p.total_q, hq), dtype=bool)
+    for i in range(len(p.seq_lens)):
+        for j in range(int(p.q_start[i + 1] - p.q_start[i])):
+            for h in range(hq):
+                reached[p.q_start[i] + j, h] = j * G + h % G < reach
+    assert (~reached).any() and reached.any()
+    assert_attention_close(got[reached], ref[reached], dtype, "reached rows")
+    assert np.isnan(got[~reached]).all()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("hq,hkv,d", SHAPES)
 @pytest.mark.parametrize("window", [0, 5, 128])
 def test_attention_ragged_small(dtype, hq, hkv, d, window):
