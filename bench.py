@@ -35,6 +35,12 @@ CALIB_BYTES = 256 << 20  # the plain elementwise kernel of --copy-calibration re
 # sources whose change invalidates a stored traffic measurement of the attention call
 KERNEL_SOURCES = ("paper_2608_24004_amd/csrc/verify_attention.hip",
                   "paper_2608_24004_amd/csrc/common.h", "paper_2608_24004_amd/build.py")
+# ... and a stored instruction count of the sampled acceptance kernel
+ACCEPT_SOURCES = ("paper_2608_24004_amd/csrc/verify_accept.hip",
+                  "paper_2608_24004_amd/csrc/common.h", "paper_2608_24004_amd/build.py")
+# vector-ALU issue peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane-instructions/s (a wave64
+# instruction holds a 16-lane SIMD for 4 cycles)
+VALU_PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9
 
 
 def log(*a):
@@ -65,10 +71,10 @@ def accept_bytes(bt) -> float:
     return float(T) * cfg.vocab * e + 4.0 * (4 * T + 3 * B + 1)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -88,6 +94,20 @@ def stored_traffic(workload: str):
     if kv.get("source_sha256", "").strip() != kernel_source_hash():
         return None
     return float(kv["traffic_bytes_per_call"])
+
+
+def stored_sample_instructions(workload: str):
+    """VALU instructions of one sample_chunks dispatch from the committed
+    counter summary, or None when there is none or the sources changed."""
+    path = os.path.join(ROOT, "profiles", "counters_verify_step_%s.md" % workload)
+    try:
+        kv = dict(l.split(":", 1) for l in open(path) if l.startswith(("accept_source_sha256:",
+                                                                     "valu_instructions_sample_chunks:")))
+    except OSError:
+        return None
+    if kv.get("accept_source_sha256", "").strip() != kernel_source_hash(ACCEPT_SOURCES):
+        return None
+    return float(kv["valu_instructions_sample_chunks"])
 
 
 def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
@@ -241,6 +261,16 @@ def accept_timing(av, bt, steps: int, aws):
         us = graph_time_us(fn, max(steps, 2 * copies))
         res[name] = {"us": us, "GBps": nbytes / (us * 1e-6) / 1e9,
                      "logits_per_ns": T * V / (us * 1e3)}
+    # the sampled call is bound by vector-ALU issue: its counted instructions
+    # (64 lanes each) per second against the issue peak
+    ninst = stored_sample_instructions(bt.cfg.name)
+    if ninst is not None:
+        sus = res["sampled_T0.7"]["us"]  # the whole call (sample_chunks + accept_scan)
+        achieved = ninst * 64 / (sus * 1e-6)
+        res["sampled_T0.7"]["roofline"] = {
+            "bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_LANE_OPS / 1e12,
+            "unit": "T VALU lane-instructions/s", "frac": achieved / VALU_PEAK_LANE_OPS,
+            "instructions": ninst}
     del lg
     return res
 
