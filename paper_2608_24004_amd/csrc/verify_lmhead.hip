@@ -6,356 +6,407 @@
 // tokens in one pass and the result equals plain greedy decoding).
 //
 // The contraction is dense (every weight row meets every scored row), so it
-// runs on MFMA: v_mfma_f32_32x32x16_bf16 with the vocabulary on the M side
-// (A = 32 weight rows x 16 hidden dims) and the scored rows on the N side
-// (B = 16 hidden dims x 32 rows).  A lane of the 32 x 32 result holds one
-// scored row (column l % 32) and 16 vocabulary entries, so most of the argmax
-// is a running compare inside the lane.
+// runs on MFMA: v_mfma_f32_16x16x32_bf16 with the vocabulary on the M side
+// (A = 16 weight rows x 32 hidden dims) and the scored rows on the N side
+// (B = 32 hidden dims x 16 rows).  A lane of a 16 x 16 result holds one
+// scored row (column l % 16) and four consecutive vocabulary entries, so most
+// of the argmax is a running compare inside the lane.
 //
-// Work split.  lmhead_argmax launches one 12-wavefront workgroup per compute
-// unit (three wavefronts per SIMD).  Workgroup w owns the vocabulary range
-// [V w / N, V (w+1) / N); wavefront (q, g) takes vocabulary quarter q of it and
-// scored-row group g (of three) of the current row chunk, and walks its
-// quarter in passes of two 32-entry tiles (the last pass may hold one).  Per
-// pass, the hidden dimension is walked in steps of 32: each step's weight rows
-// (256 = 4 quarters x 64) and scored rows (up to 288 = 3 groups x 3 tiles of
-// 32) are copied once, 16 bytes per lane, from global memory into a ring of
-// four LDS stages (three steps in flight), read from there as MFMA operands by
-// every wavefront that needs them, and accumulated in registers (2 x 3 tiles
-// of 16 floats per lane).  At the end of a pass the lane folds its logits
-// into a running (maximum, first index, first NaN) per scored row.  Every
-// weight byte is read from HBM once per row chunk; the hidden states (a few
-// MB) come from L2.  More than 288 scored rows are cut into row chunks, each
-// walking the weights again.
+// Work split.  lmhead_argmax launches one 8-wavefront workgroup per compute
+// unit (two wavefronts per SIMD).  The vocabulary is cut into 16-row tiles
+// and workgroup w owns tiles [n_tiles w / N, n_tiles (w+1) / N).  It walks
+// them in passes of at most 20 tiles (320 rows): the register file holds a
+// 320 x 288 block of fp32 logits, so every pass sees all of a row chunk's
+// scored rows at once (Qwen shapes: 37 or 38 tiles per workgroup, two passes,
+// the hidden states staged twice).  Wavefront (g, q) takes scored-row group g
+// (of two: up to 9 tiles, 144 rows) and vocabulary group q (of four: up to 5
+// tiles of the pass) and holds 5 x 9 result tiles of 4 floats per lane.
 //
-// After the last pass the wavefronts' maxima are merged into one packed
-// (order key, ~index) word per (scored row, workgroup), the format of
-// verify_accept's per-chunk partials, and the same acceptance scan finishes
-// the step.
+// Per pass the hidden dimension is walked in steps of 64.  A step's weight
+// tiles and scored-row tiles (128 contiguous bytes per row: the HBM stream
+// runs at about 5.7 TB/s with rows of this length against 3.5 TB/s with
+// 64-byte rows) are copied once, 16 bytes per lane, from global memory into
+// one of two LDS stages; every wavefront reads its MFMA operands from there.
+// While a step's products run, the next step's copies are issued between
+// them.  Only rows that exist are staged: a pass holds exactly its tiles, so
+// the weight is read from HBM once per row chunk with no padding rows.  At
+// the end of a pass each lane folds its logits into a (maximum, first index)
+// per scored row, merged across the workgroup with a 64-bit LDS max.  More
+// than 288 scored rows are cut into row chunks, each walking the workgroup's
+// weight rows again.
+//
+// After the last pass of a row chunk the workgroup stores one packed (order
+// key, ~index) word per (scored row, workgroup), the format of verify_accept's
+// per-chunk partials, and the same acceptance scan finishes the step.
 #include <type_traits>
 
 #include "common.h"
 
+// m0 is set inside the global->LDS load sequence (see dma16_if_lt); the
+// compiler reloads m0 before each of its own uses, so clobbering it there is
+// safe.
+#pragma clang diagnostic ignored "-Winline-asm"
+
 namespace averify {
 namespace {
 
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
-constexpr int kLmRowGroups = 3;                    // scored-row groups per workgroup
-constexpr int kLmWaves = 4 * kLmRowGroups;         // 4 vocabulary quarters x the row groups
-constexpr int kLmQuarters = 4;
+constexpr int kLmRowGroups = 2;                         // scored-row groups per workgroup
+constexpr int kLmVocGroups = 4;                         // vocabulary groups per workgroup
+constexpr int kLmWaves = kLmRowGroups * kLmVocGroups;   // 8
 constexpr int kLmThreads = kLmWaves * kWave;
-constexpr int kLmStep = 32;                        // hidden dims per LDS stage
-constexpr int kLmStages = 4;                       // LDS ring stages
-constexpr int kLmDepth = kLmStages - 1;            // stages in flight
-constexpr int kLmWaveRows = 64;                    // weight rows per wavefront and pass
-constexpr int kLmWRows = kLmQuarters * kLmWaveRows;  // weight rows per stage (256)
-constexpr int kLmMaxTiles = 3;                     // scored-row tiles of 32 per wavefront
-constexpr int kLmRowBytes = kLmStep * 2;           // one row of a stage: 32 bf16 = 64 bytes
+constexpr int kLmTile = 16;                             // rows per tile (MFMA M and N)
+constexpr int kLmMaxVT = 5;                             // vocabulary tiles per group and pass
+constexpr int kLmPassTiles = kLmVocGroups * kLmMaxVT;   // 20 tiles = 320 rows per pass
+constexpr int kLmMaxRT = 18 / kLmRowGroups;             // scored-row tiles per group
+constexpr int kLmChunkRows = kLmRowGroups * kLmMaxRT * kLmTile;  // 288
+constexpr int kLmMinStep = 32;                          // hidden_size granularity
+constexpr int kLmStep = 64;                             // hidden dims per LDS stage
 constexpr uint32_t kLmNone = 0xffffffffu;
 
 struct LArgs {
     int T;           // scored rows
-    int H;           // hidden size (multiple of kLmStep)
+    int H;           // hidden size (multiple of kLmMinStep)
     int V;           // vocabulary
+    int tiles;       // vocabulary tiles of 16 rows
     int nwg;         // workgroups (vocabulary ranges)
-    int chunk_rows;  // scored rows per row chunk (<= kLmRowGroups * 32 * MT)
+    int chunk_rows;  // scored rows per row chunk (<= kLmChunkRows)
     int nchunks;     // row chunks
-    int passes;      // passes of two tiles per wavefront over its vocabulary quarter
-    int nk;          // hidden steps per pass (H / kLmStep)
+    int nk;          // hidden steps per pass: ceil(H / kLmStep)
+    int tail;        // 1 if the last step holds only 32 dims (H % 64 == 32)
 };
 
-// A stage holds kLmRowGroups * MT * 32 scored rows, then 256 weight rows, each 32 bf16 = four
-// 16-byte chunks.  Chunk c of row r is stored at position c ^ f(r), f(r) =
-// 2 ((r >> 2) & 1) + ((r >> 3) & 1).  A ds_read_b128 of 32 rows at one logical
-// chunk (two chunks per row, one per half-wave) then takes gfx950's minimum of
-// four LDS cycles; measured with the LDS bank-conflict counter, the unswizzled
-// layout takes sixteen and an XOR of bits 1-3 eight.
+// A staged row holds CH 16-byte chunks.  Chunk c of tile row r (0..15) is
+// stored at position c ^ ((r >> 1) mod CH).  An operand read (lane l: row
+// l % 16, logical chunk l / 16 of the 32-dim half) then takes gfx950's minimum
+// of four LDS cycles per ds_read_b128, measured for 64- and 128-byte rows;
+// the plain layout takes twice (64-byte rows) or four times (128-byte rows) as
+// long, and so does an XOR with (r >> 2).
+template <int CH>
 __device__ __forceinline__ int swz(int r, int c) {
-    return c ^ (((r >> 2) & 1) << 1) ^ ((r >> 3) & 1);
+    return c ^ ((r >> 1) & (CH - 1));
 }
 
-// f(std::integral_constant<int, v>) for a runtime v in [0, M].
-template <int M, typename F>
-__device__ __forceinline__ void with_count(int v, F&& f) {
-    if constexpr (M == 0) {
-        f(std::integral_constant<int, 0>{});
-    } else {
-        if (v >= M) f(std::integral_constant<int, M>{});
-        else with_count<M - 1>(v, f);
+// f(std::integral_constant<int, i>) for i = 0 .. N-1
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, I + 1>(f);
     }
 }
 
-// Vocabulary quarter q [lo, hi) of workgroup w.
-__device__ __forceinline__ void wave_range(const LArgs& a, int w, int q, int& lo, int& hi) {
-    const int64_t v0 = (int64_t)a.V * w / a.nwg, v1 = (int64_t)a.V * (w + 1) / a.nwg;
-    const int64_t len = v1 - v0;
-    lo = (int)(v0 + len * q / kLmQuarters);
-    hi = (int)(v0 + len * (q + 1) / kLmQuarters);
+// A pointer every lane holds the same value of, in scalar registers.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+    const uint64_t u = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)u);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(u >> 32));
+    return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
 
-// Fold one logit into a running (maximum, first index, first NaN): logits
-// arrive in ascending vocabulary order, so a strict compare keeps the lowest
-// index among equal maxima (-0.0 == +0.0).
-__device__ __forceinline__ void fold(float x, uint32_t v, bool ok, float& best, uint32_t& bidx,
-                                     uint32_t& nidx) {
-    const bool nan = ok && x != x;
-    nidx = (nan && nidx == kLmNone) ? v : nidx;
-    const bool gt = ok && x > best;
-    best = gt ? x : best;
-    bidx = gt ? v : bidx;
+// If C < n: 16 bytes per lane from global memory at sbase + voff (a
+// wavefront-uniform base and a per-lane 32-bit byte offset, the
+// global_load_lds_dwordx4 saddr form) into LDS bytes [lds + 16 l, lds + 16 l +
+// 16) of lane l.  The test is made inside the statement, so a skipped load
+// leaves no branch in the compiler's view of the surrounding products.
+template <int C>
+__device__ __forceinline__ void dma16_if_lt(int n, uint32_t lds_wave_base, const void* sbase,
+                                            uint32_t voff) {
+    asm volatile("s_cmp_le_i32 %3, %4\n\ts_cbranch_scc1 1f\n\t"
+                 "s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2\n1:"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_wave_base)), "v"(voff),
+                   "s"(uniform_ptr(sbase)), "s"(n), "n"(C)
+                 : "memory", "m0", "scc");
 }
 
+// Fold one logit into a running (maximum, its first index): logits arrive in
+// ascending vocabulary order, so a strict compare keeps the lowest index among
+// equal maxima (-0.0 == +0.0), and the first NaN replaces any number and is
+// then kept (a NaN counts as the maximum).
+__device__ __forceinline__ void fold(float x, uint32_t v, bool ok, float& best, uint32_t& bidx) {
+    const bool take = ok && (x > best || (x != x && best == best));
+    best = take ? x : best;
+    bidx = take ? v : bidx;
+}
+
+// MT = scored-row tiles per row group (the row chunk holds at most 2 MT tiles)
 template <int MT>
 __global__ __launch_bounds__(kLmThreads)
 __attribute__((amdgpu_waves_per_eu(kLmRowGroups, kLmRowGroups)))
 void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __restrict__ wt,
                    uint64_t* __restrict__ partial) {
-    constexpr int HROWS = kLmRowGroups * MT * 32;        // scored rows per stage
-    constexpr int STAGE = (HROWS + kLmWRows) * kLmRowBytes;
-    constexpr int NI = (HROWS + kLmWRows) * 4 / kWave;   // 1 KiB global->LDS loads per stage
-    constexpr int CPT_HI = (NI + kLmWaves - 1) / kLmWaves;
-    constexpr int CPT_LO = NI / kLmWaves;
-    static_assert(NI * kWave == (HROWS + kLmWRows) * 4, "whole 1 KiB loads per stage");
-    static_assert(CPT_HI * (kLmDepth - 1) < 64, "vmcnt range");
+    constexpr int KS = kLmStep;
+    constexpr int CH = KS / 8;                            // 16-byte chunks per staged row
+    constexpr int TB = kLmTile * KS * 2;                  // bytes per staged tile (2 KiB)
+    constexpr int LPT = TB / 1024;                        // 1 KiB loads per tile
+    constexpr int KSUB = KS / 32;                         // 32-dim products per stage
+    constexpr int HT = kLmRowGroups * MT;                 // scored-row tile slots per stage
+    constexpr int STAGE = (HT + kLmPassTiles) * TB;
+    constexpr int CPT = ((HT + kLmPassTiles) * LPT + kLmWaves - 1) / kLmWaves;  // loads per wave
+    constexpr int SLOTS = KSUB * MT;                      // product groups per step
+    // load c2 is issued before product group slot_of(c2) = h MT + n: the
+    // loads are spread over the first two thirds of the step, so that they
+    // queue while the matrix cores run instead of all after the barrier
+    // (measured 459 -> 392 us on the Qwen-shaped call)
+    constexpr int SPREAD = SLOTS * 2 / 3 > 0 ? SLOTS * 2 / 3 : 1;
+    constexpr auto slot_of = [](int c2) { return c2 * SPREAD / CPT; };
+    static_assert(kLmWaves % LPT == 0, "a wavefront loads the same part of every tile");
+    static_assert(CPT < 64, "vmcnt range");
 
-    __shared__ __attribute__((aligned(16))) uint8_t stage[kLmStages][STAGE];
-    __shared__ uint64_t red[kLmQuarters][HROWS];
+    __shared__ __attribute__((aligned(1024))) uint8_t stage[2][STAGE];
 
     const int w = blockIdx.x;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);  // wavefront-uniform
-    const int c32 = lane & 31, h = lane >> 5;
-    const int cpt = wv < NI % kLmWaves || NI % kLmWaves == 0 ? CPT_HI : CPT_LO;
-    const int wq = wv % kLmQuarters;  // vocabulary quarter
-    const int wg = wv / kLmQuarters;  // row group: rows [32 MT wg, 32 MT (wg + 1)) of a chunk
+    const int r16 = lane & 15, kq = lane >> 4;
+    const int vq = wv % kLmVocGroups;  // vocabulary group
+    const int rg = wv / kLmVocGroups;  // scored-row group: tiles [MT rg, MT (rg + 1)) of a chunk
 
-    // this wavefront's vocabulary quarter and the workgroup's range
-    int vlo, vhi;
-    wave_range(a, w, wq, vlo, vhi);
-    const int wg_lo = (int)((int64_t)a.V * w / a.nwg);
-    const int wg_hi = (int)((int64_t)a.V * (w + 1) / a.nwg);
-    const int wtiles = (vhi - vlo + 31) / 32;  // this wavefront's 32-entry tiles
+    // this workgroup's vocabulary tiles and their passes
+    const int t0 = (int)((int64_t)a.tiles * w / a.nwg);
+    const int t1 = (int)((int64_t)a.tiles * (w + 1) / a.nwg);
+    const int ntw = t1 - t0;
+    const int passes = max(1, (ntw + kLmPassTiles - 1) / kLmPassTiles);
+    auto pass_tiles = [&](int p, int& pt0, int& pt) {
+        pt0 = t0 + ntw * p / passes;
+        pt = t0 + ntw * (p + 1) / passes - pt0;
+    };
+    auto chunk_tiles = [&](int c, int& r0, int& rows) {
+        r0 = c * a.chunk_rows;
+        rows = min(a.T, r0 + a.chunk_rows) - r0;
+    };
 
     const uint32_t stage_lds =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)&stage[0][0];
-    const int units = a.nchunks * a.passes * a.nk;
+    const int units = a.nchunks * passes * a.nk;
 
-    // ---- loader: unit u = (row chunk, pass, hidden step); one unit fills one
-    // stage.  Load c2 of this wavefront is stage load i = 12 c2 + wv, covering
-    // stage chunks [64 i, 64 i + 64); lane l moves chunk 64 i + l.
-    const uint16_t* src[CPT_HI];
-    int l_u = 0, l_ks = 0;
-    auto set_sources = [&](int u) {
-        const int mc = u / (a.passes * a.nk);
-        const int p = (u / a.nk) % a.passes;
-        const int r0 = mc * a.chunk_rows;
-        const int r1 = min(a.T, r0 + a.chunk_rows);
-#pragma unroll
-        for (int c2 = 0; c2 < CPT_HI; ++c2) {
-            const int i = c2 * kLmWaves + wv;
-            if (i >= NI) {  // this wavefront has one load fewer
-                src[c2] = hid;
-                continue;
-            }
-            const int pos = i * kWave + lane;        // stage chunk
-            const int row = pos >> 2, cs = pos & 3;  // stage row, stored chunk
-            const int c = swz(row, cs);              // logical chunk: dims 8c .. 8c+7
-            const uint16_t* sp;
-            if (row < HROWS) {
-                const int r = min(r0 + row, r1 - 1);  // rows past the chunk repeat its last
-                sp = hid + (int64_t)r * a.H + c * 8;
-            } else {
-                const int wr = row - HROWS;           // weight row of the stage
-                const int q = wr / kLmWaveRows, t = wr % kLmWaveRows;
-                int qlo, qhi;
-                wave_range(a, w, q, qlo, qhi);
-                int v = qlo + p * kLmWaveRows + t;
-                // rows past the quarter read the workgroup's first row again
-                // (served from cache; their results are never used)
-                if (v >= qhi) v = min(wg_lo, a.V - 1);
-                sp = wt + (int64_t)v * a.H + c * 8;
-            }
-            src[c2] = sp;
-        }
+    // ---- loader.  Unit u = (row chunk, pass, hidden step) fills one stage:
+    // its scored-row tiles into slots [0, HT) and its vocabulary tiles into
+    // slots [HT, HT + 20), two 1 KiB global->LDS loads per tile.  Stage load
+    // L (tile L / 2, part L % 2) is issued by wavefront L % 8, so a wavefront
+    // always loads the same part of its tiles: lane l moves tile row
+    // (64 part + l) / 8, stored chunk (64 part + l) % 8.  Each load reads from
+    // a wavefront-uniform base (the tile's first row at the unit's step) plus a
+    // per-lane offset; rows past the scored rows or the vocabulary repeat the
+    // last one.  In a 32-dim last step the upper four chunks repeat the lower.
+    const int jpart = wv % LPT;
+    const int lrow = (jpart * kWave + lane) / CH;
+    const int lc16 = swz<CH>(lrow, (jpart * kWave + lane) % CH) * 16;
+    const int i0 = wv / LPT;  // first tile of this wavefront; its c-th load is tile i0 + 4 c
+    constexpr int TSTEP = kLmWaves / LPT;  // tiles between a wavefront's consecutive loads
+    // the loader's unit: index, hidden step, and per (chunk, pass) the global
+    // base of this wavefront's first scored-row tile (h) and vocabulary tile
+    // (v), their LDS slots, the last row a load may read relative to each
+    // base (rows past it repeat it), and the load counts: loads c < hc are
+    // scored-row tiles, c < vc exist at all (0 once every unit is loaded)
+    int l_u = 0, l_ks = 0, l_tail = 0, l_hslot = 0, l_vslot = 0, l_hc = 0, l_vc = 0;
+    int l_hlim = 0, l_vlim = 0;
+    const uint16_t* l_hbase = hid;
+    const uint16_t* l_vbase = wt;
+    auto loader_set = [&](int u) {  // the loader's unit becomes u (< units)
+        l_u = u;
+        const int cp = u / a.nk;
+        const int ks = u - cp * a.nk;
+        l_ks = ks;
+        l_tail = a.tail && ks == a.nk - 1;
+        if (ks != 0 && u != 0) return;  // same (chunk, pass) as the previous unit
+        const int c = cp / passes, p = cp - (cp / passes) * passes;
+        int r0, rows, pt0, pt;
+        chunk_tiles(c, r0, rows);
+        pass_tiles(p, pt0, pt);
+        const int htc = (rows + kLmTile - 1) / kLmTile;
+        const int hrow = r0 + i0 * kLmTile, vrow = (pt0 - htc + i0) * kLmTile;
+        l_hbase = hid + (int64_t)hrow * a.H;
+        l_vbase = wt + (int64_t)vrow * a.H;
+        l_hslot = i0;
+        l_vslot = HT - htc + i0;
+        l_hlim = a.T - 1 - hrow;
+        l_vlim = a.V - 1 - vrow;
+        l_hc = max(0, (htc - i0 + TSTEP - 1) / TSTEP);
+        l_vc = max(0, (htc + pt - i0 + TSTEP - 1) / TSTEP);
     };
-    auto dma_unit = [&](int st) {
-        const uint32_t base = stage_lds + st * STAGE;
-        const int koff = l_ks * kLmStep;
-#pragma unroll
-        for (int c2 = 0; c2 < CPT_HI; ++c2) {
-            const int i = c2 * kLmWaves + wv;
-            if (i < NI) dma16(base + i * (kWave * 16), src[c2] + koff);
-        }
+    // per step: the loader's bases at its hidden step, the LDS addresses of
+    // its first tiles in stage st, and the lane's chunk offset
+    const uint16_t* d_hb = hid;
+    const uint16_t* d_vb = wt;
+    uint32_t d_hl = 0, d_vl = 0, d_c16 = 0;
+    int d_n = 0;
+    auto dma_prepare = [&](int st) {
+        d_hb = l_hbase + l_ks * KS;
+        d_vb = l_vbase + l_ks * KS;
+        const uint32_t sbase = stage_lds + st * STAGE + jpart * 1024;
+        d_hl = sbase + l_hslot * TB;
+        d_vl = sbase + l_vslot * TB;
+        d_c16 = (uint32_t)(l_tail ? (lc16 & 63) : lc16);
+        d_n = l_u < units ? l_vc : 0;
     };
-    // issue the loads of the loader's unit into stage st, then step the loader
-    // (it stays on the last unit, loading it again, so that every iteration
-    // issues the same number of loads)
-    auto dma_next = [&](int st) {
-        dma_unit(st);
-        if (l_u + 1 < units) {
-            ++l_u;
-            if (++l_ks == a.nk) {
-                l_ks = 0;
-                set_sources(l_u);
-            }
-        }
+    // load c2 of this wavefront for the prepared unit
+    auto dma_one = [&](auto c2c) {
+        constexpr int c2 = decltype(c2c)::value;
+        constexpr int tr = c2 * TSTEP * kLmTile;  // row of the load's tile from its base
+        const bool is_h = c2 < l_hc;
+        const uint32_t voff = (uint32_t)(min(tr + lrow, is_h ? l_hlim : l_vlim) * (a.H * 2)) + d_c16;
+        dma16_if_lt<c2>(d_n, (is_h ? d_hl : d_vl) + c2 * TSTEP * TB, is_h ? d_hb : d_vb, voff);
+    };
+    auto dma_all = [&](int st) {
+        dma_prepare(st);
+        static_for<CPT>([&](auto c2) { dma_one(c2); });
+    };
+    auto loader_next = [&]() {
+        if (l_u + 1 < units) loader_set(l_u + 1);
+        else l_u = units;
     };
 
-    // ---- running maxima per scored-row tile
-    float best[MT];
-    uint32_t bidx[MT], nidx[MT];
-#pragma unroll
-    for (int n = 0; n < MT; ++n) {
-        best[n] = -INFINITY;
-        bidx[n] = kLmNone;
-        nidx[n] = kLmNone;
-    }
+    // ---- running maxima of the row chunk, one packed (order key, ~index)
+    // word per scored row, merged with a 64-bit LDS max at the end of every
+    // pass (so that no register holds them while the products run)
+    __shared__ uint64_t row_max[kLmChunkRows];
+    for (int r = tid; r < kLmChunkRows; r += kLmThreads) row_max[r] = 0;
 
-    // row tiles of this wavefront's group that hold rows of the current chunk
-    int mtv = MT;
-    // One hidden step of a pass: NT = weight tiles of this wavefront (1 or 2),
-    // MV = row tiles holding rows of the chunk (a compile-time count, so that
-    // the step is straight-line code: every fragment of a 16-dim half is
-    // read before its products, one LDS round trip per half instead of one
-    // per row tile).
-    auto compute = [&](int st, auto& acc, auto mv) {
+    // One hidden step on stage st: NT vocabulary tiles (first tile vt0 of the
+    // pass) x MT scored-row tiles, KSUB products of 32 dims each.  The weight
+    // fragments of a 32-dim half are read once and kept; each scored-row
+    // fragment feeds NT products.  The loads of the loader's unit into the
+    // other stage are issued between the product groups.
+    auto compute = [&](int st, auto& acc, int vt0, int nt) {
         constexpr int NT = sizeof(acc) / sizeof(acc[0]);
-        constexpr int MV = decltype(mv)::value;
-        if constexpr (MV > 0) {
-            const uint8_t* hs = stage[st];
-            const uint8_t* ws = stage[st] + HROWS * kLmRowBytes;
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int cs = swz(c32, 2 * j + h) * 16;  // same swizzle for every tile row
-                bf16x8_t wf[NT], hf[MV];
-#pragma unroll
-                for (int t = 0; t < NT; ++t)
-                    wf[t] = __builtin_bit_cast(
-                        bf16x8_t, *reinterpret_cast<const uint4*>(
-                                      ws + (wq * kLmWaveRows + t * 32 + c32) * kLmRowBytes + cs));
-#pragma unroll
-                for (int n = 0; n < MV; ++n)
-                    hf[n] = __builtin_bit_cast(
-                        bf16x8_t, *reinterpret_cast<const uint4*>(
-                                      hs + ((wg * MT + n) * 32 + c32) * kLmRowBytes + cs));
-#pragma unroll
-                for (int n = 0; n < MV; ++n)
-#pragma unroll
-                    for (int t = 0; t < NT; ++t)
-                        acc[t][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[t], hf[n], acc[t][n], 0, 0, 0);
-            }
-        }
-    };
-
-    // fold a pass's logits into the running maxima: lane (h, c32) holds entry
-    // 8 (e / 4) + 4 h + e % 4 of each weight tile
-    auto end_pass = [&](int p, auto& acc) {
-        constexpr int NT = sizeof(acc) / sizeof(acc[0]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int v0 = vlo + p * kLmWaveRows + t * 32 + 4 * h;
-#pragma unroll
-            for (int n = 0; n < MT; ++n) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int v = v0 + 8 * (e >> 2) + (e & 3);
-                    fold(acc[t][n][e], (uint32_t)v, v < vhi, best[n], bidx[n], nidx[n]);
-                }
-                // one tile at a time: keeps the scheduler from moving every
-                // accumulator into vector registers at once
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-    };
-
-    // merge the four wavefronts' maxima of a row chunk and store one packed
-    // word per scored row
-    auto end_chunk = [&](int mc) {
-        const int r0 = mc * a.chunk_rows;
-        const int nrows = min(a.T, r0 + a.chunk_rows) - r0;
-#pragma unroll
-        for (int n = 0; n < MT; ++n) {
-            uint64_t pk = 0;
-            if (nidx[n] != kLmNone) pk = pack(0xffffffffu, nidx[n]);
-            else if (bidx[n] != kLmNone) pk = pack(order_key(__float_as_uint(best[n])), bidx[n]);
-            const uint64_t other = shfl_xor_u64(pk, 32);
-            pk = other > pk ? other : pk;
-            if (h == 0) red[wq][(wg * MT + n) * 32 + c32] = pk;
-            best[n] = -INFINITY;
-            bidx[n] = kLmNone;
-            nidx[n] = kLmNone;
-        }
-        lds_barrier();
-        for (int r = tid; r < nrows; r += kLmThreads) {
-            uint64_t m = red[0][r];
-#pragma unroll
-            for (int q = 1; q < kLmQuarters; ++q) m = red[q][r] > m ? red[q][r] : m;
-            // a range whose logits are all -inf reports its first entry
-            if (m == 0 && wg_lo < wg_hi) m = pack(order_key(__float_as_uint(-INFINITY)), (uint32_t)wg_lo);
-            partial[(int64_t)(r0 + r) * a.nwg + w] = m;
-        }
-        lds_barrier();
-    };
-
-    set_sources(0);
-#pragma unroll
-    for (int r = 0; r < kLmDepth; ++r) dma_next(r);
-
-    // Ring pipeline per hidden step: wait for this wavefront's loads of the
-    // step's stage, barrier (everyone's loads landed, everyone is done with
-    // the previous stage), refill the previous stage kLmDepth steps ahead,
-    // compute.  One pass walks the hidden dimension with the accumulators in
-    // registers; its tile count is fixed for the pass, so the inner loop has
-    // no branch around the products.
-    int st = 0;
-    auto step = [&]() {
-        if (cpt == CPT_HI) wait_vmcnt<CPT_HI * (kLmDepth - 1)>();
-        else wait_vmcnt<CPT_LO * (kLmDepth - 1)>();
-        lds_barrier();
-        dma_next(st == 0 ? kLmStages - 1 : st - 1);
-    };
-    auto pass = [&](int p, auto ntiles) {
-        constexpr int NT = decltype(ntiles)::value;
-        if constexpr (NT == 0) {
-            // no vocabulary left for this wavefront: keep the pipeline's pace
-            for (int ks = 0; ks < a.nk; ++ks) {
-                step();
-                st = st == kLmStages - 1 ? 0 : st + 1;
-            }
-        } else {
-            f32x16_t acc[NT][MT];
+        const int tmax = max(nt - 1, 0);
+        const uint8_t* sb = stage[st];
+        dma_prepare(st ^ 1);
+        static_for<KSUB>([&](auto hc) {
+            constexpr int h = decltype(hc)::value;
+            const int off = r16 * (CH * 16) + swz<CH>(r16, 4 * h + kq) * 16;
+            // scored-row fragment n, read by an LDS load the compiler does not
+            // see: the fragment of the next group is requested before this
+            // group's products, and one explicit wait (every LDS load but the
+            // newest has landed) makes this group's fragment ready.  The
+            // fragment passes through the wait as an operand, so the products
+            // that use it cannot be placed before the wait and the two
+            // fragments never share registers.
+            const uint32_t hbase = (uint32_t)(uintptr_t)(
+                __attribute__((address_space(3))) const uint8_t*)(sb + rg * MT * TB + off);
+            auto hread = [&](auto nc) {
+                constexpr int n = decltype(nc)::value;
+                u32x4 v;
+                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(hbase), "n"(n * TB) : "memory");
+                return v;
+            };
+            bf16x8_t wf[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t)
+                wf[t] = __builtin_bit_cast(
+                    bf16x8_t, *reinterpret_cast<const uint4*>(sb + (HT + vt0 + min(t, tmax)) * TB + off));
+            u32x4 hf[2];
+            hf[0] = hread(std::integral_constant<int, 0>{});
+            static_for<MT>([&](auto nc) {
+                constexpr int n = decltype(nc)::value;
+                static_for<CPT>([&](auto c2) {
+                    if constexpr (slot_of(decltype(c2)::value) == h * MT + n) dma_one(c2);
+                });
+                if constexpr (n + 1 < MT) {
+                    hf[(n + 1) & 1] = hread(std::integral_constant<int, n + 1>{});
+                    asm volatile("s_waitcnt lgkmcnt(1)" : "+v"(hf[n & 1]) : : "memory");
+                } else {
+                    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(hf[n & 1]) : : "memory");
+                }
+                const bf16x8_t hv = __builtin_bit_cast(bf16x8_t, hf[n & 1]);
 #pragma unroll
-                for (int n = 0; n < MT; ++n) acc[t][n] = f32x16_t{};
-            auto walk = [&](auto mv) {
-                int ks = 0;
-                do {  // nk >= 1
-                    step();
-                    compute(st, acc, mv);
-                    st = st == kLmStages - 1 ? 0 : st + 1;
-                } while (++ks < a.nk);
-            };
-            with_count<MT>(mtv, walk);
-            end_pass(p, acc);
+                for (int t = 0; t < NT; ++t)
+                    acc[t][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[t], hv, acc[t][n], 0, 0, 0);
+            });
+        });
+    };
+
+    // fold a pass's logits into the chunk's maxima: lane (kq, r16) holds
+    // vocabulary entries 4 kq .. 4 kq + 3 of each tile for scored row r16
+    auto end_pass = [&](auto& acc, int vbase, int nt) {
+        constexpr int NT = sizeof(acc) / sizeof(acc[0]);
+#pragma unroll
+        for (int n = 0; n < MT; ++n) {
+            float best = -INFINITY;
+            uint32_t bidx = kLmNone;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int v0 = vbase + t * kLmTile + 4 * kq;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int v = v0 + e;
+                    fold(acc[t][n][e], (uint32_t)v, t < nt && v < a.V, best, bidx);
+                }
+            }
+            uint64_t pk = bidx != kLmNone ? pack(order_key(__float_as_uint(best)), bidx) : 0;
+            uint64_t o = shfl_xor_u64(pk, 16);
+            pk = o > pk ? o : pk;
+            o = shfl_xor_u64(pk, 32);
+            pk = o > pk ? o : pk;
+            if (kq == 0 && pk != 0) atomicMax(reinterpret_cast<unsigned long long*>(&row_max[(rg * MT + n) * kLmTile + r16]),
+                                                (unsigned long long)pk);
         }
     };
-    for (int mc = 0; mc < a.nchunks; ++mc) {
-        {
-            const int r0 = mc * a.chunk_rows;
-            const int left = min(a.T, r0 + a.chunk_rows) - r0 - wg * MT * 32;
-            mtv = __builtin_amdgcn_readfirstlane(min(MT, max(0, (left + 31) / 32)));
+
+    // store the chunk's maxima, one packed word per scored row, and clear
+    // them for the next chunk
+    auto end_chunk = [&](int c) {
+        int r0, rows;
+        chunk_tiles(c, r0, rows);
+        lds_barrier();  // every wavefront's last pass is merged
+        const int v_first = t0 * kLmTile;
+        for (int r = tid; r < kLmChunkRows; r += kLmThreads) {
+            uint64_t m = row_max[r];
+            row_max[r] = 0;
+            // a range whose logits are all -inf reports its first entry
+            if (m == 0 && ntw > 0) m = pack(order_key(__float_as_uint(-INFINITY)), (uint32_t)v_first);
+            if (r < rows) partial[(int64_t)(r0 + r) * a.nwg + w] = m;
         }
-        for (int p = 0; p < a.passes; ++p) {
-            const int nt = min(2, max(0, wtiles - 2 * p));
-            if (nt == 2) pass(p, std::integral_constant<int, 2>{});
-            else if (nt == 1) pass(p, std::integral_constant<int, 1>{});
-            else pass(p, std::integral_constant<int, 0>{});
+    };
+
+    // Double-buffered pipeline per hidden step: wait for this wavefront's
+    // loads of the step's stage, barrier (everyone's loads landed, everyone is
+    // done with the other stage), then compute on this stage while the next
+    // unit's loads go into the other one.
+    loader_set(0);
+    dma_all(0);
+    loader_next();
+    int st = 0;
+    for (int c = 0; c < a.nchunks; ++c) {
+        for (int p = 0; p < passes; ++p) {
+            int pt0, pt;
+            pass_tiles(p, pt0, pt);
+            const int vt0 = pt * vq / kLmVocGroups;
+            const int nt = pt * (vq + 1) / kLmVocGroups - vt0;
+            // every wavefront runs kLmMaxVT vocabulary tiles; a group with
+            // fewer repeats its last one (or the pass's first) and folds only
+            // its own
+            f32x4_t acc[kLmMaxVT][MT];
+#pragma unroll
+            for (int t = 0; t < kLmMaxVT; ++t)
+#pragma unroll
+                for (int n = 0; n < MT; ++n) acc[t][n] = f32x4_t{};
+            int ks = 0;
+            do {  // nk >= 1
+                wait_vmcnt<0>();
+                lds_barrier();
+                if (a.tail && ks == a.nk - 1) {
+                    // a 32-dim last step: clear dims 32..63 of every staged row
+                    // (they repeat dims 0..31), so the upper half adds exact zeros
+                    for (int e = tid; e < (HT + kLmPassTiles) * kLmTile * 4; e += kLmThreads) {
+                        const int row = e >> 2;
+                        *reinterpret_cast<uint4*>(stage[st] + row * (CH * 16) +
+                                                  swz<CH>(row & 15, 4 + (e & 3)) * 16) = make_uint4(0, 0, 0, 0);
+                    }
+                    lds_barrier();
+                }
+                compute(st, acc, vt0, nt);
+                loader_next();
+                st ^= 1;
+            } while (++ks < a.nk);
+            end_pass(acc, (pt0 + vt0) * kLmTile, nt);
         }
-        end_chunk(mc);
+        end_chunk(c);
     }
     // no global->LDS load may still be writing when the workgroup's LDS is freed
     wait_vmcnt<0>();
@@ -366,6 +417,22 @@ void launch_lmhead(const LArgs& a, const uint16_t* hid, const uint16_t* wt, uint
                    hipStream_t stream) {
     hipLaunchKernelGGL(lmhead_argmax<MT>, dim3(a.nwg), dim3(kLmThreads), 0, stream, a, hid, wt,
                        partial);
+}
+
+// launch lmhead_argmax<MT> for the smallest instantiated MT >= mt
+template <int M>
+bool launch_lmhead_mt(int mt, const LArgs& a, const uint16_t* hid, const uint16_t* wt,
+                      uint64_t* partial, hipStream_t stream) {
+    if constexpr (M == 0) {
+        return false;
+    } else {
+        if (mt > M / 2 || M == 1) {
+            if (mt > M) return false;
+            launch_lmhead<M>(a, hid, wt, partial, stream);
+            return true;
+        }
+        return launch_lmhead_mt<M / 2>(mt, a, hid, wt, partial, stream);
+    }
 }
 
 struct LmPlan {
@@ -385,7 +452,7 @@ int lm_cus() {
 }
 
 bool lm_args_ok(int32_t num_seqs, int32_t total_q, int32_t hidden_size, int64_t vocab) {
-    return num_seqs >= 0 && total_q >= 0 && hidden_size >= kLmStep && hidden_size % kLmStep == 0 &&
+    return num_seqs >= 0 && total_q >= 0 && hidden_size >= kLmMinStep && hidden_size % kLmMinStep == 0 &&
            vocab >= 1 && vocab < (int64_t)0x7fffffff;
 }
 
@@ -395,16 +462,14 @@ LmPlan plan_lmhead(int32_t total_q, int32_t hidden_size, int64_t vocab) {
     a.T = total_q;
     a.H = hidden_size;
     a.V = (int)vocab;
-    a.nwg = (int)std::min<int64_t>(lm_cus(), vocab);
-    constexpr int max_rows = kLmRowGroups * kLmMaxTiles * 32;
-    a.nchunks = std::max(1, (total_q + max_rows - 1) / max_rows);
+    a.tiles = (int)((vocab + kLmTile - 1) / kLmTile);
+    a.nwg = std::min(lm_cus(), a.tiles);
+    a.nchunks = std::max(1, (total_q + kLmChunkRows - 1) / kLmChunkRows);
     a.chunk_rows = std::max(1, (total_q + a.nchunks - 1) / a.nchunks);
-    pl.mt = (a.chunk_rows + kLmRowGroups * 32 - 1) / (kLmRowGroups * 32);
-    const int64_t wg_len = (vocab + a.nwg - 1) / a.nwg;
-    const int64_t q_len = (wg_len + kLmQuarters - 1) / kLmQuarters;
-    const int64_t tiles = (q_len + 31) / 32;
-    a.passes = (int)std::max<int64_t>(1, (tiles + 1) / 2);
-    a.nk = hidden_size / kLmStep;
+    const int htc = (a.chunk_rows + kLmTile - 1) / kLmTile;
+    pl.mt = (htc + kLmRowGroups - 1) / kLmRowGroups;
+    a.nk = (hidden_size + kLmStep - 1) / kLmStep;
+    a.tail = hidden_size % kLmStep != 0;
     pl.partial_bytes = align_up((size_t)total_q * a.nwg * sizeof(uint64_t), 256);
     pl.argmax_bytes = align_up((size_t)total_q * sizeof(int32_t), 256);
     return pl;
@@ -448,12 +513,7 @@ extern "C" int verify_lmhead_accept(int32_t num_seqs, int32_t total_q, int32_t h
     if (total_q > 0) {
         const uint16_t* hs = static_cast<const uint16_t*>(hidden);
         const uint16_t* ws = static_cast<const uint16_t*>(weight);
-        switch (pl.mt) {
-            case 1: launch_lmhead<1>(pl.a, hs, ws, partial, stream); break;
-            case 2: launch_lmhead<2>(pl.a, hs, ws, partial, stream); break;
-            case 3: launch_lmhead<3>(pl.a, hs, ws, partial, stream); break;
-            default: return VERIFY_EUNSUPPORTED;
-        }
+        if (!launch_lmhead_mt<kLmMaxRT>(pl.mt, pl.a, hs, ws, partial, stream)) return VERIFY_EUNSUPPORTED;
         if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
     }
     return launch_accept_scan(num_seqs, q_start, tokens, partial, pl.a.nwg, am, accept_len,
