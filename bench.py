@@ -547,11 +547,43 @@ def summarize_counters(paths) -> None:
             names[r["Dispatch_Id"]] = m.group(1)
         for (d, c), v in per.items():
             agg[names[d]][c].append(v)
+    mean = {k: {c: sum(v) / len(v) for c, v in agg[k].items()} for k in agg}
+    # derived figures per dispatch: the counters sum over the chip's 8 XCDs and
+    # 1024 SIMDs; SQ_WAVE_CYCLES and the SQ wait/active counters count in units
+    # of 4 cycles
+    need = ("GRBM_GUI_ACTIVE", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_WAIT_INST_ANY",
+            "SQ_WAVE_CYCLES", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT", "TA_BUSY_avr", "TCC_HIT_sum",
+            "TCC_MISS_sum", "SQ_WAVES", "SQ_INSTS_SALU", "SQ_INSTS_VMEM", "SQ_INSTS_MFMA")
+    print("| kernel | cycles per XCD | waves | MFMA busy | VALU busy | waiting | LDS active | "
+          "LDS conflict share | TA busy | L2 hit | VALU / SALU / VMEM / MFMA instr per wave |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
+    for k in sorted(mean):
+        m = mean[k]
+        if not all(c in m for c in need):
+            continue
+        cyc = m["GRBM_GUI_ACTIVE"] / 8
+        waves = max(m["SQ_WAVES"], 1.0)
+        print("| `%s` | %.0f | %.0f | %.2f | %.2f | %.2f | %.2f | %.2f | %.2f | %.2f | %.0f / %.0f / %.0f / %.0f |" % (
+            k, cyc, m["SQ_WAVES"], m["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / cyc,
+            4 * m["SQ_INSTS_VALU"] / 1024 / cyc, m["SQ_WAIT_INST_ANY"] / max(m["SQ_WAVE_CYCLES"], 1.0),
+            m["SQ_LDS_IDX_ACTIVE"] / 256 / cyc, m["SQ_LDS_BANK_CONFLICT"] / max(m["SQ_LDS_IDX_ACTIVE"], 1.0),
+            m["TA_BUSY_avr"] / cyc, m["TCC_HIT_sum"] / max(m["TCC_HIT_sum"] + m["TCC_MISS_sum"], 1.0),
+            m["SQ_INSTS_VALU"] / waves, m["SQ_INSTS_SALU"] / waves, m["SQ_INSTS_VMEM"] / waves,
+            m["SQ_INSTS_MFMA"] / waves))
+    if "sample_chunks" in mean and "SQ_INSTS_VALU" in mean["sample_chunks"]:
+        print()
+        print("valu_instructions_sample_chunks: %.0f" % mean["sample_chunks"]["SQ_INSTS_VALU"])
+        print("accept_source_sha256: %s" % kernel_source_hash(ACCEPT_SOURCES))
+    print()
+    print("Raw means per dispatch:")
+    print()
+    print("```")
     for k in sorted(agg):
         print("%s:" % k)
         for c in sorted(agg[k]):
             v = agg[k][c]
             print("  %-28s %16.1f  (mean of %d dispatches)" % (c, sum(v) / len(v), len(v)))
+    print("```")
 
 
 def main():
