@@ -13,14 +13,26 @@
 // of the argmax is a running compare inside the lane.
 //
 // Work split.  lmhead_argmax launches one 8-wavefront workgroup per compute
-// unit (two wavefronts per SIMD).  The vocabulary is cut into 16-row tiles
-// and workgroup w owns tiles [n_tiles w / N, n_tiles (w+1) / N).  It walks
-// them in passes of at most 20 tiles (320 rows): the register file holds a
-// 320 x 288 block of fp32 logits, so every pass sees all of a row chunk's
-// scored rows at once (Qwen shapes: 37 or 38 tiles per workgroup, two passes,
-// the hidden states staged twice).  Wavefront (g, q) takes scored-row group g
-// (of two: up to 9 tiles, 144 rows) and vocabulary group q (of four: up to 5
-// tiles of the pass) and holds 5 x 9 result tiles of 4 floats per lane.
+// unit (two wavefronts per SIMD).  The vocabulary is cut into 16-row tiles.
+// Workgroups form groups, one per XCD (workgroup w runs on XCD w % 8), and
+// each group owns one eighth of the tiles.  Up to 288 scored rows, a group's
+// 32 workgroups split its tiles evenly.  Beyond that the rows are cut into
+// row chunks of at most 288: the group's workgroups are dealt out over the
+// chunks, and the workgroups of different chunks split the group's tiles the
+// same way, so the workgroups that share a vocabulary range run side by side
+// on one XCD and the weight they read comes from HBM once, then from that
+// XCD's L2 (Qwen shapes at 2152 rows: eight chunks of 269 rows, 3.55 ms ->
+// 2.35 ms against eight workgroup-private passes over the weight).  Rows
+// beyond 288 per workgroup of a group are walked in rounds, one after
+// another.  Where workgroups land on XCDs decides only the speed.
+//
+// A workgroup walks its tiles in passes of at most 20 tiles (320 rows): the
+// register file holds a 320 x 288 block of fp32 logits, so every pass sees all
+// of its chunk's scored rows at once (Qwen shapes: 37 or 38 tiles per
+// workgroup, two passes, the hidden states staged twice).  Wavefront (g, q)
+// takes scored-row group g (of two: up to 9 tiles, 144 rows) and vocabulary
+// group q (of four: up to 5 tiles of the pass) and holds 5 x 9 result tiles of
+// 4 floats per lane.
 //
 // Per pass the hidden dimension is walked in steps of 64.  A step's weight
 // tiles and scored-row tiles (128 contiguous bytes per row: the HBM stream
@@ -28,16 +40,16 @@
 // 64-byte rows) are copied once, 16 bytes per lane, from global memory into
 // one of two LDS stages; every wavefront reads its MFMA operands from there.
 // While a step's products run, the next step's copies are issued between
-// them.  Only rows that exist are staged: a pass holds exactly its tiles, so
-// the weight is read from HBM once per row chunk with no padding rows.  At
-// the end of a pass each lane folds its logits into a (maximum, first index)
-// per scored row, merged across the workgroup with a 64-bit LDS max.  More
-// than 288 scored rows are cut into row chunks, each walking the workgroup's
-// weight rows again.
+// them.  Only rows that exist are staged: a pass holds exactly its tiles, with
+// no padding rows.  At the end of a pass each lane folds its logits into a
+// (maximum, first index) per scored row, merged across the workgroup with a
+// 64-bit LDS max.
 //
 // After the last pass of a row chunk the workgroup stores one packed (order
-// key, ~index) word per (scored row, workgroup), the format of verify_accept's
-// per-chunk partials, and the same acceptance scan finishes the step.
+// key, ~index) word per scored row in its column of the row's partials (the
+// format of verify_accept's per-chunk partials; a column no workgroup owns
+// holds 0, which loses every comparison), and the same acceptance scan
+// finishes the step.
 #include <type_traits>
 
 #include "common.h"
@@ -64,16 +76,20 @@ constexpr int kLmMaxRT = 18 / kLmRowGroups;             // scored-row tiles per 
 constexpr int kLmChunkRows = kLmRowGroups * kLmMaxRT * kLmTile;  // 288
 constexpr int kLmMinStep = 32;                          // hidden_size granularity
 constexpr int kLmStep = 64;                             // hidden dims per LDS stage
-constexpr uint32_t kLmNone = 0xffffffffu;
+constexpr int kLmXcds = 8;                              // MI355X: 8 XCDs, each with its own L2
 
 struct LArgs {
     int T;           // scored rows
     int H;           // hidden size (multiple of kLmMinStep)
     int V;           // vocabulary
     int tiles;       // vocabulary tiles of 16 rows
-    int nwg;         // workgroups (vocabulary ranges)
-    int chunk_rows;  // scored rows per row chunk (<= kLmChunkRows)
-    int nchunks;     // row chunks
+    int nwg;         // workgroups
+    int xg;          // workgroup groups, one vocabulary slice each (workgroup w is in group w % xg)
+    int kg;          // workgroups per group (nwg / xg)
+    int nc;          // row chunks per round; a group's workgroups are dealt out over them
+    int rounds;      // rounds of row chunks, walked one after another
+    int round_rows;  // scored rows per round (the last round may hold fewer)
+    int ncols;       // partial words per scored row: xg * ceil(kg / nc)
     int nk;          // hidden steps per pass: ceil(H / kLmStep)
     int tail;        // 1 if the last step holds only 32 dims (H % 64 == 32)
 };
@@ -122,14 +138,31 @@ __device__ __forceinline__ void dma16_if_lt(int n, uint32_t lds_wave_base, const
                  : "memory", "m0", "scc");
 }
 
-// Fold one logit into a running (maximum, its first index): logits arrive in
+// Whether logit x replaces the running maximum best: logits arrive in
 // ascending vocabulary order, so a strict compare keeps the lowest index among
 // equal maxima (-0.0 == +0.0), and the first NaN replaces any number and is
-// then kept (a NaN counts as the maximum).
-__device__ __forceinline__ void fold(float x, uint32_t v, bool ok, float& best, uint32_t& bidx) {
-    const bool take = ok && (x > best || (x != x && best == best));
-    best = take ? x : best;
-    bidx = take ? v : bidx;
+// then kept (a NaN counts as the maximum).  !(x <= best) is x > best or x a
+// NaN; once best is a NaN nothing replaces it.  Bitwise operators keep it
+// free of branches.
+__device__ __forceinline__ bool fold_take(float x, float best) {
+    return !(x <= best) & (best == best);
+}
+
+// Largest of v over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the four lanes that
+// hold one scored row of a 16 x 16 result tile).  Each permlane swap exchanges
+// half of the wavefront between its two operands; with both operands equal,
+// lane l gets the values of l and l ^ 32 (l ^ 16), in an order that is the
+// same for both halves of the word.
+__device__ __forceinline__ uint64_t max4_u64(uint64_t v) {
+    auto both = [](uint64_t x, auto swap) {
+        const auto lo = swap((uint32_t)x);
+        const auto hi = swap((uint32_t)(x >> 32));
+        const uint64_t c0 = ((uint64_t)hi[0] << 32) | lo[0];
+        const uint64_t c1 = ((uint64_t)hi[1] << 32) | lo[1];
+        return c0 > c1 ? c0 : c1;
+    };
+    v = both(v, [](uint32_t u) { return __builtin_amdgcn_permlane32_swap(u, u, false, false); });
+    return both(v, [](uint32_t u) { return __builtin_amdgcn_permlane16_swap(u, u, false, false); });
 }
 
 // MT = scored-row tiles per row group (the row chunk holds at most 2 MT tiles)
@@ -166,23 +199,40 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     const int vq = wv % kLmVocGroups;  // vocabulary group
     const int rg = wv / kLmVocGroups;  // scored-row group: tiles [MT rg, MT (rg + 1)) of a chunk
 
-    // this workgroup's vocabulary tiles and their passes
-    const int t0 = (int)((int64_t)a.tiles * w / a.nwg);
-    const int t1 = (int)((int64_t)a.tiles * (w + 1) / a.nwg);
+    // This workgroup's place: group x (one per XCD when the launch fills
+    // them: consecutive workgroups go to consecutive XCDs), row chunk c of
+    // every round, and j-th of the group's nc_w workgroups on that chunk.  The
+    // group's vocabulary slice is cut into nc_w ranges; the workgroups of
+    // different chunks that share a range run side by side on one XCD, so the
+    // weight they read is fetched from HBM once and served from that XCD's L2
+    // to the others.  Chunk c holds a share of a round's rows proportional to
+    // nc_w, which gives every workgroup the same work.
+    const int x = w % a.xg, k = w / a.xg;
+    const int c_w = k % a.nc, j_w = k / a.nc;
+    const int full = a.kg / a.nc, rem = a.kg % a.nc;
+    const int nc_w = full + (c_w < rem ? 1 : 0);            // workgroups of chunk c_w in the group
+    const int s_w = c_w * full + min(c_w, rem);             // of chunks before it
+    const int nmax = full + (rem ? 1 : 0);
+    const int x0 = (int)((int64_t)a.tiles * x / a.xg), x1 = (int)((int64_t)a.tiles * (x + 1) / a.xg);
+    const int t0 = x0 + (int)((int64_t)(x1 - x0) * j_w / nc_w);
+    const int t1 = x0 + (int)((int64_t)(x1 - x0) * (j_w + 1) / nc_w);
     const int ntw = t1 - t0;
+    const int col = x * nmax + j_w;  // this workgroup's partial word of a row
     const int passes = max(1, (ntw + kLmPassTiles - 1) / kLmPassTiles);
     auto pass_tiles = [&](int p, int& pt0, int& pt) {
         pt0 = t0 + ntw * p / passes;
         pt = t0 + ntw * (p + 1) / passes - pt0;
     };
-    auto chunk_tiles = [&](int c, int& r0, int& rows) {
-        r0 = c * a.chunk_rows;
-        rows = min(a.T, r0 + a.chunk_rows) - r0;
+    auto chunk_tiles = [&](int rnd, int& r0, int& rows) {
+        const int base = rnd * a.round_rows;
+        const int64_t tr = min(a.T - base, a.round_rows);
+        r0 = base + (int)(tr * s_w / a.kg);
+        rows = base + (int)(tr * (s_w + nc_w) / a.kg) - r0;
     };
 
     const uint32_t stage_lds =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)&stage[0][0];
-    const int units = a.nchunks * passes * a.nk;
+    const int units = a.rounds * passes * a.nk;
 
     // ---- loader.  Unit u = (row chunk, pass, hidden step) fills one stage:
     // its scored-row tiles into slots [0, HT) and its vocabulary tiles into
@@ -274,50 +324,70 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     // other stage are issued between the product groups.
     auto compute = [&](int st, auto& acc, int vt0, int nt) {
         constexpr int NT = sizeof(acc) / sizeof(acc[0]);
+        constexpr int G = KSUB * MT;  // product groups of the step
         const int tmax = max(nt - 1, 0);
         const uint8_t* sb = stage[st];
         dma_prepare(st ^ 1);
-        static_for<KSUB>([&](auto hc) {
-            constexpr int h = decltype(hc)::value;
-            const int off = r16 * (CH * 16) + swz<CH>(r16, 4 * h + kq) * 16;
-            // scored-row fragment n, read by an LDS load the compiler does not
-            // see: the fragment of the next group is requested before this
-            // group's products, and one explicit wait (every LDS load but the
-            // newest has landed) makes this group's fragment ready.  The
-            // fragment passes through the wait as an operand, so the products
-            // that use it cannot be placed before the wait and the two
-            // fragments never share registers.
-            const uint32_t hbase = (uint32_t)(uintptr_t)(
-                __attribute__((address_space(3))) const uint8_t*)(sb + rg * MT * TB + off);
-            auto hread = [&](auto nc) {
-                constexpr int n = decltype(nc)::value;
-                u32x4 v;
-                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(hbase), "n"(n * TB) : "memory");
-                return v;
-            };
-            bf16x8_t wf[NT];
+        const int off0 = r16 * (CH * 16);
+        auto woff = [&](int h) { return off0 + swz<CH>(r16, 4 * h + kq) * 16; };
+        // scored-row fragment of group g (32-dim half g / MT, tile g % MT),
+        // read by an LDS load the compiler does not see
+        const uint32_t hrow = (uint32_t)(uintptr_t)(
+            __attribute__((address_space(3))) const uint8_t*)(sb + rg * MT * TB + off0);
+        auto hread = [&](auto gc) {
+            constexpr int g = decltype(gc)::value;
+            constexpr int h = g / MT, n = g % MT;
+            const uint32_t addr = hrow + (uint32_t)(swz<CH>(r16, 4 * h + kq) * 16);
+            u32x4 v;
+            asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(n * TB) : "memory");
+            return v;
+        };
+        auto wread = [&](int h, int t) {
+            return __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const uint4*>(sb + (HT + vt0 + min(t, tmax)) * TB + woff(h)));
+        };
+        bf16x8_t wf[NT];
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
-                wf[t] = __builtin_bit_cast(
-                    bf16x8_t, *reinterpret_cast<const uint4*>(sb + (HT + vt0 + min(t, tmax)) * TB + off));
-            u32x4 hf[2];
-            hf[0] = hread(std::integral_constant<int, 0>{});
-            static_for<MT>([&](auto nc) {
-                constexpr int n = decltype(nc)::value;
-                static_for<CPT>([&](auto c2) {
-                    if constexpr (slot_of(decltype(c2)::value) == h * MT + n) dma_one(c2);
-                });
-                if constexpr (n + 1 < MT) {
-                    hf[(n + 1) & 1] = hread(std::integral_constant<int, n + 1>{});
-                    asm volatile("s_waitcnt lgkmcnt(1)" : "+v"(hf[n & 1]) : : "memory");
-                } else {
-                    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(hf[n & 1]) : : "memory");
+        for (int t = 0; t < NT; ++t) wf[t] = wread(0, t);
+        // three scored-row fragments in flight: the fragment of group g + 2 is
+        // requested before group g's products, and an explicit wait (every
+        // LDS load but the two newest has landed) makes group g's ready.  The
+        // fragment passes through the wait as an operand, so the products
+        // that use it cannot be placed before the wait.
+        u32x4 hf[4];
+        hf[0] = hread(std::integral_constant<int, 0>{});
+        if constexpr (G > 1) hf[1] = hread(std::integral_constant<int, 1>{});
+        if constexpr (G > 2) hf[2] = hread(std::integral_constant<int, 2>{});
+        static_for<G>([&](auto gc) {
+            constexpr int g = decltype(gc)::value;
+            constexpr int h = g / MT, n = g % MT;
+            static_for<CPT>([&](auto c2) {
+                if constexpr (slot_of(decltype(c2)::value) == g) dma_one(c2);
+            });
+            if constexpr (g + 3 < G) {
+                hf[(g + 3) % 4] = hread(std::integral_constant<int, g + 3>{});
+                asm volatile("s_waitcnt lgkmcnt(3)" : "+v"(hf[g % 4]) : : "memory");
+            } else if constexpr (g + 2 < G) {
+                asm volatile("s_waitcnt lgkmcnt(2)" : "+v"(hf[g % 4]) : : "memory");
+            } else if constexpr (g + 1 < G) {
+                asm volatile("s_waitcnt lgkmcnt(1)" : "+v"(hf[g % 4]) : : "memory");
+            } else {
+                asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(hf[g % 4]) : : "memory");
+            }
+            const bf16x8_t hv = __builtin_bit_cast(bf16x8_t, hf[g % 4]);
+            if constexpr (n == MT - 1 && h + 1 < KSUB) {
+                // the half's last group: each weight fragment is reloaded for
+                // the next half right after its last product
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    acc[t][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[t], hv, acc[t][n], 0, 0, 0);
+                    wf[t] = wread(h + 1, t);
                 }
-                const bf16x8_t hv = __builtin_bit_cast(bf16x8_t, hf[n & 1]);
+            } else {
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
                     acc[t][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[t], hv, acc[t][n], 0, 0, 0);
-            });
+            }
         });
     };
 
@@ -328,21 +398,24 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
 #pragma unroll
         for (int n = 0; n < MT; ++n) {
             float best = -INFINITY;
-            uint32_t bidx = kLmNone;
+            int bloc = -1;  // t * 16 + e of the maximum
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const int v0 = vbase + t * kLmTile + 4 * kq;
+                // entries past the pass's tiles or the vocabulary count as -inf,
+                // which replaces nothing
+                const bool full = t < nt && vbase + (t + 1) * kLmTile <= a.V;  // wavefront-uniform
+                const int lim = t < nt ? a.V - (vbase + t * kLmTile + 4 * kq) : 0;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int v = v0 + e;
-                    fold(acc[t][n][e], (uint32_t)v, t < nt && v < a.V, best, bidx);
+                    float x = acc[t][n][e];
+                    if (!full) x = e < lim ? x : -INFINITY;
+                    const bool take = fold_take(x, best);
+                    best = take ? x : best;
+                    bloc = take ? t * kLmTile + e : bloc;
                 }
             }
-            uint64_t pk = bidx != kLmNone ? pack(order_key(__float_as_uint(best)), bidx) : 0;
-            uint64_t o = shfl_xor_u64(pk, 16);
-            pk = o > pk ? o : pk;
-            o = shfl_xor_u64(pk, 32);
-            pk = o > pk ? o : pk;
+            uint64_t pk = bloc >= 0 ? pack(order_key(__float_as_uint(best)), (uint32_t)(vbase + 4 * kq + bloc)) : 0;
+            pk = max4_u64(pk);
             if (kq == 0 && pk != 0) atomicMax(reinterpret_cast<unsigned long long*>(&row_max[(rg * MT + n) * kLmTile + r16]),
                                                 (unsigned long long)pk);
         }
@@ -360,7 +433,13 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
             row_max[r] = 0;
             // a range whose logits are all -inf reports its first entry
             if (m == 0 && ntw > 0) m = pack(order_key(__float_as_uint(-INFINITY)), (uint32_t)v_first);
-            if (r < rows) partial[(int64_t)(r0 + r) * a.nwg + w] = m;
+            if (r < rows) {
+                uint64_t* pr = partial + (int64_t)(r0 + r) * a.ncols;
+                pr[col] = m;
+                // a chunk with fewer workgroups than nmax leaves the group's
+                // last word of its rows to its last workgroup: the neutral 0
+                if (nc_w < nmax && j_w == nc_w - 1) pr[col + 1] = 0;
+            }
         }
     };
 
@@ -372,7 +451,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     dma_all(0);
     loader_next();
     int st = 0;
-    for (int c = 0; c < a.nchunks; ++c) {
+    for (int rnd = 0; rnd < a.rounds; ++rnd) {
         for (int p = 0; p < passes; ++p) {
             int pt0, pt;
             pass_tiles(p, pt0, pt);
@@ -406,7 +485,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
             } while (++ks < a.nk);
             end_pass(acc, (pt0 + vt0) * kLmTile, nt);
         }
-        end_chunk(c);
+        end_chunk(rnd);
     }
     // no global->LDS load may still be writing when the workgroup's LDS is freed
     wait_vmcnt<0>();
@@ -419,19 +498,18 @@ void launch_lmhead(const LArgs& a, const uint16_t* hid, const uint16_t* wt, uint
                        partial);
 }
 
-// launch lmhead_argmax<MT> for the smallest instantiated MT >= mt
-template <int M>
+// launch lmhead_argmax<mt> (1 <= mt <= kLmMaxRT)
+template <int M = 1>
 bool launch_lmhead_mt(int mt, const LArgs& a, const uint16_t* hid, const uint16_t* wt,
                       uint64_t* partial, hipStream_t stream) {
-    if constexpr (M == 0) {
+    if constexpr (M > kLmMaxRT) {
         return false;
     } else {
-        if (mt > M / 2 || M == 1) {
-            if (mt > M) return false;
+        if (mt == M) {
             launch_lmhead<M>(a, hid, wt, partial, stream);
             return true;
         }
-        return launch_lmhead_mt<M / 2>(mt, a, hid, wt, partial, stream);
+        return launch_lmhead_mt<M + 1>(mt, a, hid, wt, partial, stream);
     }
 }
 
@@ -464,13 +542,27 @@ LmPlan plan_lmhead(int32_t total_q, int32_t hidden_size, int64_t vocab) {
     a.V = (int)vocab;
     a.tiles = (int)((vocab + kLmTile - 1) / kLmTile);
     a.nwg = std::min(lm_cus(), a.tiles);
-    a.nchunks = std::max(1, (total_q + kLmChunkRows - 1) / kLmChunkRows);
-    a.chunk_rows = std::max(1, (total_q + a.nchunks - 1) / a.nchunks);
-    const int htc = (a.chunk_rows + kLmTile - 1) / kLmTile;
-    pl.mt = (htc + kLmRowGroups - 1) / kLmRowGroups;
+    a.xg = a.nwg % kLmXcds == 0 ? kLmXcds : 1;
+    a.kg = a.nwg / a.xg;
+    // rounds: as few as hold the rows (a round's chunks hold at most 288 rows
+    // each, one chunk per workgroup of a group at most)
+    const int64_t per_round = (int64_t)kLmChunkRows * a.kg;
+    a.rounds = (int)std::max<int64_t>(1, (total_q + per_round - 1) / per_round);
+    a.round_rows = std::max(1, (int)(((int64_t)total_q + a.rounds - 1) / a.rounds));
+    // chunks per round: the fewest whose largest chunk (the workgroups of a
+    // group dealt out over them, rows in proportion) fits 288 rows
+    int rows_max = a.round_rows;
+    for (a.nc = 1; a.nc <= a.kg; ++a.nc) {
+        const int nmax = (a.kg + a.nc - 1) / a.nc;
+        rows_max = (int)(((int64_t)a.round_rows * nmax + a.kg - 1) / a.kg);
+        if (rows_max <= kLmChunkRows) break;
+    }
+    a.ncols = a.xg * ((a.kg + a.nc - 1) / a.nc);
+    const int htc = (rows_max + kLmTile - 1) / kLmTile;
+    pl.mt = std::max(1, (htc + kLmRowGroups - 1) / kLmRowGroups);
     a.nk = (hidden_size + kLmStep - 1) / kLmStep;
     a.tail = hidden_size % kLmStep != 0;
-    pl.partial_bytes = align_up((size_t)total_q * a.nwg * sizeof(uint64_t), 256);
+    pl.partial_bytes = align_up((size_t)total_q * a.ncols * sizeof(uint64_t), 256);
     pl.argmax_bytes = align_up((size_t)total_q * sizeof(int32_t), 256);
     return pl;
 }
@@ -513,9 +605,9 @@ extern "C" int verify_lmhead_accept(int32_t num_seqs, int32_t total_q, int32_t h
     if (total_q > 0) {
         const uint16_t* hs = static_cast<const uint16_t*>(hidden);
         const uint16_t* ws = static_cast<const uint16_t*>(weight);
-        if (!launch_lmhead_mt<kLmMaxRT>(pl.mt, pl.a, hs, ws, partial, stream)) return VERIFY_EUNSUPPORTED;
+        if (!launch_lmhead_mt(pl.mt, pl.a, hs, ws, partial, stream)) return VERIFY_EUNSUPPORTED;
         if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
     }
-    return launch_accept_scan(num_seqs, q_start, tokens, partial, pl.a.nwg, am, accept_len,
+    return launch_accept_scan(num_seqs, q_start, tokens, partial, pl.a.ncols, am, accept_len,
                               num_emitted, emitted, stream);
 }

@@ -94,9 +94,12 @@ CASES = [
     ([17, 0, 33, 15], 128, 5003),
     ([65], 96, 777),
     ([9] * 32, 256, 3001),               # 288 rows: one full row chunk
-    ([9] * 32 + [1], 128, 3001),         # 289 rows: a second chunk of one row
+    ([9] * 32 + [1], 128, 3001),         # 289 rows: two chunks of 144 and 145 rows
     ([9] * 36, 256, 3001),               # 324 rows: two row chunks
-    ([33] * 21, 64, 2048),               # 693 rows: three row chunks
+    ([33] * 21, 64, 2048),               # 693 rows, 128 tiles: three chunks with 6, 5 and 5
+                                         # workgroups per XCD group (a column left neutral)
+    ([7] * 111, 64, 777),                # 777 rows, 49 tiles: one group of 49 workgroups, 3 chunks
+    ([33] * 300, 64, 4096),              # 9900 rows: two rounds of 32 chunks
     ([3, 8, 1], 2880, 4099),
 ]
 
