@@ -125,7 +125,8 @@ typedef struct verify_attn_params {
  *                (they size the launch; tighter bounds launch less idle work).
  *                Rows of a request with n_i > max_q_len that the launch does
  *                not reach (verify_attention_plan gives the reach: rows j with
- *                j * (Hq/Hkv) + h % (Hq/Hkv) below info[3] * info[2]) are not
+ *                j * (Hq/Hkv) + h % (Hq/Hkv) below the row groups times the
+ *                rows per group of the request's row class) are not
  *                computed: their outputs are written as quiet NaN.
  *   workspace    device scratch of at least the size returned by
  *                verify_attention_workspace_size() for the same (params,
@@ -145,18 +146,23 @@ int verify_attention(const verify_attn_params *params, int32_t total_q, int32_t 
  * verify_attention_plan -- the work decomposition verify_attention would use
  * for the same arguments, for tests and tools (nothing is launched).
  *
+ *   info     int32[VERIFY_ATTN_PLAN_INFO], written in full (unused entries 0)
  *   info[0]  1: bf16 persistent MFMA schedule, 0: fp32 split-K VALU kernel
- *   bf16:    info[1] workgroups sharing the units, info[2] query rows per row
- *            group, info[3] row groups per (request, KV head) at most,
- *            info[4] fixed units per workgroup (0: equal shares).  A unit is
- *            one 16-token block of one (request, KV head, row group) pair;
- *            units are numbered request by request, then KV head, then row
- *            group, then block, and workgroup w owns units
- *            [U w / N, U (w + 1) / N) of the U units (N = min(info[1], U)).
+ *   bf16:    info[5] row classes (1 or 2), one persistent launch each; a
+ *            request whose Hq/Hkv * n_i is at most info[10] is in class 0,
+ *            the others in class 1.  Class 0 in info[1..4], class 1 in
+ *            info[6..9]: workgroups, query rows per row group, row groups
+ *            per (request, KV head) at most, fixed units per workgroup (0:
+ *            equal shares).  A unit is one 16-token block of one (request, KV
+ *            head, row group) pair of the class's requests; units are
+ *            numbered request by request, then KV head, then row group, then
+ *            block, and workgroup w owns units [U w / N, U (w + 1) / N) of the
+ *            class's U units (N = min(workgroups, U)).
  *   fp32:    info[1] splits per request at most, info[2] query rows per work
  *            item, info[3] row groups, info[4] KV blocks per split.
  * Same argument checks as verify_attention_workspace_size.
  */
+#define VERIFY_ATTN_PLAN_INFO 11
 int verify_attention_plan(const verify_attn_params *params, int32_t total_q, int32_t max_q_len,
                           int32_t max_seq_len, int32_t *info);
 

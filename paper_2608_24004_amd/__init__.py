@@ -219,16 +219,25 @@ def attention_workspace_size(q, k_cache, block_tables, *, max_q_len: int, max_se
     return int(n.value)
 
 
+PLAN_INFO = 11  # entries of verify_attention_plan's info array
+
+
 def attention_plan(q, k_cache, block_tables, *, max_q_len: int, max_seq_len: int,
                    sliding_window: int = 0, scale: float = 0.0, kv_split_blocks: int = 0) -> dict:
     """The work decomposition verify_attention would use (nothing is launched)."""
     p = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
-    info = (ctypes.c_int32 * 5)()
+    info = (ctypes.c_int32 * PLAN_INFO)()
     _check(library().verify_attention_plan(ctypes.byref(p), int(q.shape[0]), int(max_q_len),
                                            int(max_seq_len), info), "verify_attention_plan")
-    keys = (("mfma", "workgroups", "rows_per_group", "row_groups", "units_per_workgroup") if info[0]
-            else ("mfma", "splits", "rows_per_item", "row_groups", "split_blocks"))
-    return dict(zip(keys, [int(x) for x in info]))
+    v = [int(x) for x in info]
+    if not v[0]:
+        return dict(zip(("mfma", "splits", "rows_per_item", "row_groups", "split_blocks"), v[:5]))
+    # bf16: one persistent launch per row class (requests by Hq/Hkv * n_i)
+    keys = ("workgroups", "rows_per_group", "row_groups", "units_per_workgroup")
+    classes = [dict(zip(keys, v[1:5]), rows_lo=0, rows_hi=v[10])]
+    if v[5] > 1:
+        classes.append(dict(zip(keys, v[6:10]), rows_lo=v[10] + 1, rows_hi=2 ** 31 - 1))
+    return dict(mfma=1, classes=classes, **classes[0])
 
 
 def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, max_q_len: int,

@@ -311,6 +311,8 @@ struct PArgs {
     int nwg;              // workgroups of the persistent launch
     int spb;              // > 0: fixed number of units per workgroup
     int inline_sched;     // 1: attn_persist computes the unit offsets itself
+    int rows_lo, rows_hi; // the launch's row class: requests whose group * n_i lies in
+                          // [rows_lo, rows_hi]; the others belong to another launch
     const float* sinks;   // [Hq] sink logits (natural-log units) or null
 };
 
@@ -355,6 +357,7 @@ __device__ __forceinline__ ReqGeom req_geom(const PArgs& a, const int32_t* __res
     r.nb = max(0, b_hi - r.b_lo);
     const int rows = a.group * max(0, r.n);
     r.rg = min(a.rg_max, (rows + a.rows_per_group - 1) / a.rows_per_group);
+    if (rows < a.rows_lo || rows > a.rows_hi) r.rg = 0;  // another launch's request
     return r;
 }
 
@@ -369,6 +372,7 @@ __device__ void mark_unreached_rows(const PArgs& a, const int32_t* __restrict__ 
     for (int i = t0; i < a.num_seqs; i += nt) {
         const int q0 = q_start[i];
         const int rows = a.group * (q_start[i + 1] - q0);
+        if (rows < a.rows_lo || rows > a.rows_hi) continue;
         for (int rr = reach; rr < rows; ++rr)
             for (int g = 0; g < a.hkv; ++g) {
                 const int64_t hrow = (int64_t)(q0 + rr / a.group) * a.hq + g * a.group + rr % a.group;
@@ -1033,15 +1037,35 @@ struct AttnPlan {
     int row_groups;
     size_t part_o_bytes;
     size_t part_lse_bytes;
-    // MFMA path
-    int nw, tpw;      // wavefronts per workgroup, 16-row tiles per wavefront
-    int rg_max;       // row groups per (request, KV head)
-    int nwg;          // persistent workgroups
-    int spb;          // fixed units per workgroup (0: equal shares)
-    int64_t slots;    // partial slots
-    size_t unit_bytes, slot_o_bytes, slot_lse_bytes;
+    // MFMA path: one persistent launch per row class
+    struct Class {
+        int nw, tpw;          // wavefronts per workgroup, 16-row tiles per wavefront
+        int rg_max;           // row groups per (request, KV head)
+        int nwg;              // persistent workgroups
+        int spb;              // fixed units per workgroup (0: equal shares)
+        int rows_lo, rows_hi; // requests with Hq/Hkv * n_i in [rows_lo, rows_hi]
+        int64_t slots;        // partial slots
+        size_t off;           // workspace offset of the class's arrays
+        size_t unit_bytes, slot_o_bytes, slot_lse_bytes;
+    };
+    int nclass;
+    Class cls[2];
     size_t total_bytes;
 };
+
+// Batches whose requests carry up to this many query rows per KV head (three
+// 16-row tiles) and more than that run in two launches, each with its own
+// kernel shape (see make_plan).
+constexpr int kShortClassRows = 48;
+
+// A launch whose workgroups would each own more than this many units (each
+// unit a 16-token block of 8 KiB at head dim 128, so about 3 ms of streaming)
+// launches up to eight times the resident workgroups: the hardware hands the
+// next workgroup to whichever compute unit frees a slot first, so faster
+// compute units take more of the work (long-context batch: 10.06 -> 9.10 ms at
+// eight times; at the short Qwen and DSK calls the extra start-ups cost more
+// than the balance gains).
+constexpr int64_t kOversubUnits = 4096;
 
 // KV blocks in flight per workgroup.  Three (a 32 KiB ring at D = 128) lets
 // four workgroups share a compute unit's 160 KiB of LDS; the four-wavefront
@@ -1135,6 +1159,62 @@ int resident_wgs() {
     return v;
 }
 
+// Kernel shape (wavefronts per workgroup, tiles per wavefront) for row groups
+// of up to `tiles` 16-row tiles.  A single tile goes to single-wavefront
+// workgroups: every wavefront is an independent worker with its own LDS ring
+// and no barrier.  More rows use NW wavefronts sharing one ring (NW divides
+// the 16-byte chunks of a block, 512 at D = 128 and 256 at D = 64, so every
+// thread loads alike).  At D = 128 a wavefront takes two tiles once there are
+// three or more: fewer wavefronts per block mean fewer barriers and more
+// workgroups per compute unit, which is what hides the per-block latency of
+// the online softmax.  Rows beyond the shape's reach are split into row
+// groups, each walking the request's KV again.
+void pick_shape(int head_dim, int64_t tiles, int64_t nb_max, int& nw, int& tpw) {
+    if (tiles <= 1) {
+        nw = 1;
+        tpw = 1;
+    } else if (head_dim == 128) {
+        nw = tiles <= 4 ? 2 : 4;
+        tpw = tiles == 2 ? 1 : 2;
+        if (tiles == 3 && nb_max >= 64) { nw = 1; tpw = 3; }
+    } else {
+        nw = tiles <= 2 ? 2 : 4;
+        tpw = (int)std::min<int64_t>(4, (tiles + nw - 1) / nw);
+        if (tiles == 5 && nb_max >= 64) { nw = 1; tpw = 5; }
+    }
+}
+
+// The persistent launch of one row class: requests with rows_lo <= Hq/Hkv *
+// n_i <= rows_hi, of which no request has more than `rows` rows.
+int plan_class(const verify_attn_params* p, int64_t rows, int64_t nb_max, int rows_lo, int rows_hi,
+               AttnPlan::Class& c) {
+    c = AttnPlan::Class{};
+    pick_shape(p->head_dim, (rows + 15) / 16, nb_max, c.nw, c.tpw);
+    c.rows_lo = rows_lo;
+    c.rows_hi = rows_hi;
+    const int64_t per = (int64_t)c.nw * c.tpw * 16;
+    c.rg_max = (int)((rows + per - 1) / per);
+    const int64_t pairs = (int64_t)std::max(1, p->num_seqs) * p->num_kv_heads * c.rg_max;
+    const int64_t units_max = pairs * nb_max;
+    if (units_max >= (int64_t)1 << 31) return VERIFY_EUNSUPPORTED;
+    c.spb = p->kv_split_blocks;
+    if (c.spb > 0) {
+        c.nwg = (int)std::min<int64_t>((units_max + c.spb - 1) / c.spb, (int64_t)1 << 30);
+    } else {
+        int res = 0;
+        if (!with_shape(p->head_dim, c.nw, c.tpw, [&](auto sh) { res = resident_wgs<decltype(sh)>(); }))
+            return VERIFY_EUNSUPPORTED;
+        const int64_t resident = (int64_t)device_cus() * res;
+        const int64_t mult = std::min<int64_t>(8, std::max<int64_t>(1, units_max / resident / kOversubUnits));
+        c.nwg = (int)(resident * mult);
+    }
+    c.slots = pairs + c.nwg;
+    c.unit_bytes = align_up(sizeof(int32_t) * ((size_t)std::max(1, p->num_seqs) + 1), 256);
+    c.slot_o_bytes = align_up((size_t)c.slots * per * p->head_dim * sizeof(float), 256);
+    c.slot_lse_bytes = align_up((size_t)c.slots * per * sizeof(float), 256);
+    return VERIFY_OK;
+}
+
 int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
               int32_t max_seq_len, AttnPlan* out) {
     AttnPlan pl{};
@@ -1148,47 +1228,31 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
     const int64_t rows = (int64_t)G * std::max(1, max_q_len);
     pl.mfma = p->dtype == VERIFY_BF16;
     if (pl.mfma) {
-        // A single tile goes to single-wavefront workgroups: every wavefront is
-        // an independent worker with its own LDS ring and no barrier.  More
-        // rows use NW wavefronts sharing one ring (NW divides the 16-byte
-        // chunks of a block, 512 at D = 128 and 256 at D = 64, so every thread
-        // loads alike).  At D = 128 a wavefront takes two tiles once there are
-        // three or more: fewer wavefronts per block mean fewer barriers and
-        // more workgroups per compute unit, which is what hides the per-block
-        // latency of the online softmax.  Rows beyond the shape's reach are
-        // split into row groups, each walking the request's KV again.
-        const int64_t tiles = (rows + 15) / 16;
-        if (tiles <= 1) {
-            pl.nw = 1;
-            pl.tpw = 1;
-        } else if (p->head_dim == 128) {
-            pl.nw = tiles <= 4 ? 2 : 4;
-            pl.tpw = tiles == 2 ? 1 : 2;
-            if (tiles == 3 && nb_max >= 64) { pl.nw = 1; pl.tpw = 3; }
+        // One launch sized by the largest request.  At head dim 128, when that
+        // takes the four-wavefront shape (five tiles or more), the requests
+        // of up to three tiles get a launch of their own with the shape of
+        // three tiles: the four-wavefront shape streams 5.4 TB/s on pairs of
+        // one tile but 4.2 TB/s on pairs of eight, and 5.9-6.0 TB/s on pairs
+        // of three in the three-tile shape (long contexts), so mixing draft
+        // lengths in one launch runs every pair at about the slow rate.
+        int rc;
+        if (p->head_dim == 128 && (rows + 15) / 16 >= 5) {
+            pl.nclass = 2;
+            rc = plan_class(p, kShortClassRows, nb_max, 0, kShortClassRows, pl.cls[0]);
+            if (rc == VERIFY_OK)
+                rc = plan_class(p, rows, nb_max, kShortClassRows + 1, INT32_MAX, pl.cls[1]);
         } else {
-            pl.nw = tiles <= 2 ? 2 : 4;
-            pl.tpw = (int)std::min<int64_t>(4, (tiles + pl.nw - 1) / pl.nw);
-            if (tiles == 5 && nb_max >= 64) { pl.nw = 1; pl.tpw = 5; }
+            pl.nclass = 1;
+            rc = plan_class(p, rows, nb_max, 0, INT32_MAX, pl.cls[0]);
         }
-        const int64_t per = (int64_t)pl.nw * pl.tpw * 16;
-        pl.rg_max = (int)((rows + per - 1) / per);
-        const int64_t pairs = (int64_t)std::max(1, p->num_seqs) * p->num_kv_heads * pl.rg_max;
-        const int64_t units_max = pairs * nb_max;
-        if (units_max >= (int64_t)1 << 31) return VERIFY_EUNSUPPORTED;
-        pl.spb = p->kv_split_blocks;
-        if (pl.spb > 0) {
-            pl.nwg = (int)std::min<int64_t>((units_max + pl.spb - 1) / pl.spb, (int64_t)1 << 30);
-        } else {
-            int res = 0;
-            if (!with_shape(p->head_dim, pl.nw, pl.tpw, [&](auto sh) { res = resident_wgs<decltype(sh)>(); }))
-                return VERIFY_EUNSUPPORTED;
-            pl.nwg = device_cus() * res;
+        if (rc != VERIFY_OK) return rc;
+        size_t off = 0;
+        for (int k = 0; k < pl.nclass; ++k) {
+            AttnPlan::Class& c = pl.cls[k];
+            c.off = off;
+            off += c.unit_bytes + c.slot_o_bytes + c.slot_lse_bytes;
         }
-        pl.slots = pairs + pl.nwg;
-        pl.unit_bytes = align_up(sizeof(int32_t) * ((size_t)std::max(1, p->num_seqs) + 1), 256);
-        pl.slot_o_bytes = align_up((size_t)pl.slots * per * p->head_dim * sizeof(float), 256);
-        pl.slot_lse_bytes = align_up((size_t)pl.slots * per * sizeof(float), 256);
-        pl.total_bytes = pl.unit_bytes + pl.slot_o_bytes + pl.slot_lse_bytes;
+        pl.total_bytes = off;
     } else {
         int sb = p->kv_split_blocks;
         if (sb == 0) {
@@ -1216,7 +1280,7 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
 
 // Schedule pass, then the persistent kernel of the plan's shape, then the
 // merge of partial slots.  Returns false if the plan names no known shape.
-bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan& pl, int head_dim,
+bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan::Class& pl, int head_dim,
                     int max_rows, hipStream_t stream) {
     return with_shape(head_dim, pl.nw, pl.tpw, [&](auto sh) {
         using S = decltype(sh);
@@ -1297,10 +1361,6 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         m.seq_lens = seq_lens;
         m.q_start = q_start;
         m.out = static_cast<uint16_t*>(out);
-        char* ws = static_cast<char*>(workspace);
-        m.unit_start = reinterpret_cast<int32_t*>(ws);
-        m.slot_o = reinterpret_cast<float*>(ws + pl.unit_bytes);
-        m.slot_lse = reinterpret_cast<float*>(ws + pl.unit_bytes + pl.slot_o_bytes);
         PArgs a{};
         a.num_seqs = p.num_seqs;
         a.hq = p.num_q_heads;
@@ -1312,15 +1372,27 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         a.max_seq_len = max_seq_len;
         a.scale_log2 = scale * kLog2e;
         a.inv_scale_log2 = a.scale_log2 > 0.f ? 1.f / a.scale_log2 : 0.f;
-        a.rows_per_group = pl.nw * pl.tpw * 16;
-        a.rg_max = pl.rg_max;
-        a.nwg = pl.nwg;
-        a.spb = pl.spb;
         a.inline_sched = p.num_seqs <= kInlineSchedSeqs;
         a.sinks = sinks;
         const int64_t max_rows = (int64_t)a.group * std::max(1, max_q_len);
-        if (!launch_persist(a, m, pl, p.head_dim, (int)std::min<int64_t>(max_rows, 1 << 30), stream))
-            return VERIFY_EUNSUPPORTED;
+        // one launch per row class, one after another on the stream; each
+        // writes only its own requests' outputs
+        for (int k = 0; k < pl.nclass; ++k) {
+            const AttnPlan::Class& c = pl.cls[k];
+            char* ws = static_cast<char*>(workspace) + c.off;
+            m.unit_start = reinterpret_cast<int32_t*>(ws);
+            m.slot_o = reinterpret_cast<float*>(ws + c.unit_bytes);
+            m.slot_lse = reinterpret_cast<float*>(ws + c.unit_bytes + c.slot_o_bytes);
+            a.rows_per_group = c.nw * c.tpw * 16;
+            a.rg_max = c.rg_max;
+            a.nwg = c.nwg;
+            a.spb = c.spb;
+            a.rows_lo = c.rows_lo;
+            a.rows_hi = c.rows_hi;
+            const int64_t class_rows = std::min<int64_t>(max_rows, c.rows_hi);
+            if (!launch_persist(a, m, c, p.head_dim, (int)std::min<int64_t>(class_rows, 1 << 30), stream))
+                return VERIFY_EUNSUPPORTED;
+        }
         return check_launch();
     }
 
@@ -1362,12 +1434,19 @@ extern "C" int verify_attention_plan(const verify_attn_params* params, int32_t t
     AttnPlan pl;
     rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl);
     if (rc != VERIFY_OK) return rc;
+    for (int k = 0; k < VERIFY_ATTN_PLAN_INFO; ++k) info[k] = 0;
     if (pl.mfma) {
         info[0] = 1;
-        info[1] = pl.nwg;
-        info[2] = pl.nw * pl.tpw * 16;
-        info[3] = pl.rg_max;
-        info[4] = pl.spb;
+        info[5] = pl.nclass;
+        for (int k = 0; k < pl.nclass; ++k) {
+            const AttnPlan::Class& c = pl.cls[k];
+            int32_t* d = k == 0 ? info + 1 : info + 6;
+            d[0] = c.nwg;
+            d[1] = c.nw * c.tpw * 16;
+            d[2] = c.rg_max;
+            d[3] = c.spb;
+        }
+        info[10] = pl.nclass > 1 ? pl.cls[0].rows_hi : INT32_MAX;
     } else {
         info[0] = 0;
         info[1] = pl.max_splits;

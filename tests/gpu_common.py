@@ -101,30 +101,45 @@ def pair_schedule(batch, layer, plan):
     """(request, KV head, row group) pairs of the persistent bf16 schedule and
     whether a workgroup range boundary cuts each one (its first and last KV
     blocks belong to different workgroups), from the plan verify_attention
-    reports: the unit numbering and the equal-share ranges it documents."""
+    reports: one launch per row class, each with the unit numbering and the
+    equal-share ranges it documents over the class's requests."""
     cfg = batch.cfg
     G = cfg.num_q_heads // cfg.num_kv_heads
-    rpg, rg_max, nwg = plan["rows_per_group"], plan["row_groups"], plan["workgroups"]
     n = np.diff(batch.q_start).astype(np.int64)
     S = batch.seq_lens.astype(np.int64)
     W = layer.window
     key_lo = np.maximum(0, S - n - W + 1) if W > 0 else np.zeros_like(S)
     nb = np.maximum(0, (S + 15) // 16 - key_lo // 16)
-    rg = np.minimum(rg_max, (G * n + rpg - 1) // rpg)
-    units = cfg.num_kv_heads * rg * nb
-    start = np.concatenate([[0], np.cumsum(units)])
-    U = int(start[-1])
-    N = min(nwg, max(U, 1))
-    owner = lambda u: ((u + 1) * N - 1) // max(U, 1)
     pairs = []
-    for i in range(len(n)):
-        for g in range(cfg.num_kv_heads):
-            for r in range(int(rg[i])):
-                if nb[i] == 0:
-                    continue
-                ps = int(start[i]) + (g * int(rg[i]) + r) * int(nb[i])
-                pairs.append((i, g, r, owner(ps) != owner(ps + int(nb[i]) - 1)))
+    for cls in plan.get("classes", [plan]):
+        rpg, rg_max, nwg = cls["rows_per_group"], cls["row_groups"], cls["workgroups"]
+        lo, hi = cls.get("rows_lo", 0), cls.get("rows_hi", 2 ** 31 - 1)
+        inside = (G * n >= lo) & (G * n <= hi)
+        rg = np.where(inside, np.minimum(rg_max, (G * n + rpg - 1) // rpg), 0)
+        units = cfg.num_kv_heads * rg * nb
+        start = np.concatenate([[0], np.cumsum(units)])
+        U = int(start[-1])
+        N = min(nwg, max(U, 1))
+        owner = lambda u: ((u + 1) * N - 1) // max(U, 1)
+        for i in range(len(n)):
+            for g in range(cfg.num_kv_heads):
+                for r in range(int(rg[i])):
+                    if nb[i] == 0:
+                        continue
+                    ps = int(start[i]) + (g * int(rg[i]) + r) * int(nb[i])
+                    pairs.append((i, g, r, owner(ps) != owner(ps + int(nb[i]) - 1)))
     return pairs
+
+
+def row_reach(plan, rows):
+    """Local rows (Hq/Hkv * j + h % (Hq/Hkv)) the launch computes for a request
+    with `rows` of them: its row class's row groups times rows per group."""
+    if not plan["mfma"]:
+        return plan["row_groups"] * plan["rows_per_item"]
+    for cls in plan["classes"]:
+        if cls["rows_lo"] <= rows <= cls["rows_hi"]:
+            return cls["row_groups"] * cls["rows_per_group"]
+    raise AssertionError("no row class holds %d rows" % rows)
 
 
 def pair_vectors(batch, pair, rows_per_group):

@@ -17,7 +17,7 @@ import oracle
 import paper_2608_24004_amd as av
 import workload
 from gpu_common import (NEAR_TIE, assert_attention_close, compact_for_rows, gpu_attention,
-                        oracle_accept_all, pair_schedule, to_host_f64)
+                        oracle_accept_all, pair_schedule, row_reach, to_host_f64)
 from helpers import Paged, random_paged
 
 pytestmark = pytest.mark.gpu
@@ -175,13 +175,14 @@ def test_attention_rows_past_max_q_len(dtype, hq, hkv, d, split):
                         max_q_len=max_q_len, max_seq_len=int(p.seq_lens.max()), split=split)
     plan = av.attention_plan(dv["q"], dv["kc"], dv["bt"], max_q_len=max_q_len,
                              max_seq_len=int(p.seq_lens.max()), kv_split_blocks=split)
-    reach = plan["row_groups"] * (plan["rows_per_group"] if plan["mfma"] else plan["rows_per_item"])
     got = to_host_f64(out)
     ref = oracle.attention(**p.oracle_args())
     G = hq // hkv
     reached = np.zeros((p.total_q, hq), dtype=bool)
     for i in range(len(p.seq_lens)):
-        for j in range(int(p.q_start[i + 1] - p.q_start[i])):
+        n_i = int(p.q_start[i + 1] - p.q_start[i])
+        reach = row_reach(plan, G * n_i)
+        for j in range(n_i):
             for h in range(hq):
                 reached[p.q_start[i] + j, h] = j * G + h % G < reach
     assert (~reached).any() and reached.any()
