@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10500
+    assert av.abi_version() == 10600
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
