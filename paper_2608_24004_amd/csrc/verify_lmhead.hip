@@ -26,13 +26,14 @@
 // beyond 288 per workgroup of a group are walked in rounds, one after
 // another.  Where workgroups land on XCDs decides only the speed.
 //
-// A workgroup walks its tiles in passes of at most 20 tiles (320 rows): the
-// register file holds a 320 x 288 block of fp32 logits, so every pass sees all
-// of its chunk's scored rows at once (Qwen shapes: 37 or 38 tiles per
-// workgroup, two passes, the hidden states staged twice).  Wavefront (g, q)
-// takes scored-row group g (of two: up to 9 tiles, 144 rows) and vocabulary
-// group q (of four: up to 5 tiles of the pass) and holds 5 x 9 result tiles of
-// 4 floats per lane.
+// A workgroup walks its tiles in passes: the register file holds the pass's
+// block of fp32 logits, so every pass sees all of its chunk's scored rows at
+// once.  Wavefront (g, q) takes scored-row group g (of two: MT tiles, up to 9)
+// and vocabulary group q (of four: NT tiles of the pass) and holds NT x MT
+// result tiles of 4 floats per lane; NT is 5, or 6 where that packs the
+// workgroup's tiles into fewer slots (kLmNT).
+// Qwen shapes: MT 9, NT 5, passes of 20 tiles (320 x 288 logits), 37 or 38
+// tiles per workgroup, two passes, the hidden states staged twice.
 //
 // Per pass the hidden dimension is walked in steps of 64.  A step's weight
 // tiles and scored-row tiles (128 contiguous bytes per row: the HBM stream
@@ -70,10 +71,19 @@ constexpr int kLmVocGroups = 4;                         // vocabulary groups per
 constexpr int kLmWaves = kLmRowGroups * kLmVocGroups;   // 8
 constexpr int kLmThreads = kLmWaves * kWave;
 constexpr int kLmTile = 16;                             // rows per tile (MFMA M and N)
-constexpr int kLmMaxVT = 5;                             // vocabulary tiles per group and pass
-constexpr int kLmPassTiles = kLmVocGroups * kLmMaxVT;   // 20 tiles = 320 rows per pass
+constexpr int kLmStageTiles = 38;                       // 2 KiB tiles per LDS stage at most
 constexpr int kLmMaxRT = 18 / kLmRowGroups;             // scored-row tiles per group
 constexpr int kLmChunkRows = kLmRowGroups * kLmMaxRT * kLmTile;  // 288
+
+// Vocabulary tiles per wavefront and pass (NT): 5, or 6 for 5 to 7 scored-row
+// tiles per wavefront (MT), where the two LDS stages (2 MT + 4 NT tiles of 2 KiB
+// each, 38 at most) and the accumulators (4 NT MT registers, 180 at most) hold
+// it.  Every pass runs NT tiles per wavefront whether or not the workgroup has
+// that many left, so the launch takes the NT with the fewest tile slots
+// (passes x NT; plan_lmhead).  DSK shapes (192-row chunks, 62.6 tiles per
+// workgroup): NT 6 in three passes against NT 5 in four, 478 -> 410 us.
+constexpr int kLmNT = 5;
+constexpr bool lm_wide_ok(int mt) { return mt >= 5 && mt <= 7; }
 constexpr int kLmMinStep = 32;                          // hidden_size granularity
 constexpr int kLmStep = 64;                             // hidden dims per LDS stage
 constexpr int kLmXcds = 8;                              // MI355X: 8 XCDs, each with its own L2
@@ -165,8 +175,9 @@ __device__ __forceinline__ uint64_t max4_u64(uint64_t v) {
     return both(v, [](uint32_t u) { return __builtin_amdgcn_permlane16_swap(u, u, false, false); });
 }
 
-// MT = scored-row tiles per row group (the row chunk holds at most 2 MT tiles)
-template <int MT>
+// MT = scored-row tiles per row group (the row chunk holds at most 2 MT
+// tiles), NT = vocabulary tiles per wavefront and pass
+template <int MT, int NT>
 __global__ __launch_bounds__(kLmThreads)
 __attribute__((amdgpu_waves_per_eu(kLmRowGroups, kLmRowGroups)))
 void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __restrict__ wt,
@@ -177,8 +188,10 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     constexpr int LPT = TB / 1024;                        // 1 KiB loads per tile
     constexpr int KSUB = KS / 32;                         // 32-dim products per stage
     constexpr int HT = kLmRowGroups * MT;                 // scored-row tile slots per stage
-    constexpr int STAGE = (HT + kLmPassTiles) * TB;
-    constexpr int CPT = ((HT + kLmPassTiles) * LPT + kLmWaves - 1) / kLmWaves;  // loads per wave
+    constexpr int PT = kLmVocGroups * NT;                 // vocabulary tiles per pass
+    constexpr int STAGE = (HT + PT) * TB;
+    constexpr int CPT = ((HT + PT) * LPT + kLmWaves - 1) / kLmWaves;  // loads per wave
+    static_assert(HT + PT <= kLmStageTiles && 4 * NT * MT <= 180, "stages and accumulators");
     constexpr int SLOTS = KSUB * MT;                      // product groups per step
     // load c2 is issued before product group slot_of(c2) = h MT + n: the
     // loads are spread over the first two thirds of the step, so that they
@@ -218,7 +231,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     const int t1 = x0 + (int)((int64_t)(x1 - x0) * (j_w + 1) / nc_w);
     const int ntw = t1 - t0;
     const int col = x * nmax + j_w;  // this workgroup's partial word of a row
-    const int passes = max(1, (ntw + kLmPassTiles - 1) / kLmPassTiles);
+    const int passes = max(1, (ntw + PT - 1) / PT);
     auto pass_tiles = [&](int p, int& pt0, int& pt) {
         pt0 = t0 + ntw * p / passes;
         pt = t0 + ntw * (p + 1) / passes - pt0;
@@ -236,7 +249,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
 
     // ---- loader.  Unit u = (row chunk, pass, hidden step) fills one stage:
     // its scored-row tiles into slots [0, HT) and its vocabulary tiles into
-    // slots [HT, HT + 20), two 1 KiB global->LDS loads per tile.  Stage load
+    // slots [HT, HT + PT), two 1 KiB global->LDS loads per tile.  Stage load
     // L (tile L / 2, part L % 2) is issued by wavefront L % 8, so a wavefront
     // always loads the same part of its tiles: lane l moves tile row
     // (64 part + l) / 8, stored chunk (64 part + l) % 8.  Each load reads from
@@ -323,7 +336,6 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     // fragment feeds NT products.  The loads of the loader's unit into the
     // other stage are issued between the product groups.
     auto compute = [&](int st, auto& acc, int vt0, int nt) {
-        constexpr int NT = sizeof(acc) / sizeof(acc[0]);
         constexpr int G = KSUB * MT;  // product groups of the step
         const int tmax = max(nt - 1, 0);
         const uint8_t* sb = stage[st];
@@ -394,7 +406,6 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     // fold a pass's logits into the chunk's maxima: lane (kq, r16) holds
     // vocabulary entries 4 kq .. 4 kq + 3 of each tile for scored row r16
     auto end_pass = [&](auto& acc, int vbase, int nt) {
-        constexpr int NT = sizeof(acc) / sizeof(acc[0]);
 #pragma unroll
         for (int n = 0; n < MT; ++n) {
             float best = -INFINITY;
@@ -457,12 +468,12 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
             pass_tiles(p, pt0, pt);
             const int vt0 = pt * vq / kLmVocGroups;
             const int nt = pt * (vq + 1) / kLmVocGroups - vt0;
-            // every wavefront runs kLmMaxVT vocabulary tiles; a group with
+            // every wavefront runs NT vocabulary tiles; a group with
             // fewer repeats its last one (or the pass's first) and folds only
             // its own
-            f32x4_t acc[kLmMaxVT][MT];
+            f32x4_t acc[NT][MT];
 #pragma unroll
-            for (int t = 0; t < kLmMaxVT; ++t)
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
                 for (int n = 0; n < MT; ++n) acc[t][n] = f32x4_t{};
             int ks = 0;
@@ -472,7 +483,7 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
                 if (a.tail && ks == a.nk - 1) {
                     // a 32-dim last step: clear dims 32..63 of every staged row
                     // (they repeat dims 0..31), so the upper half adds exact zeros
-                    for (int e = tid; e < (HT + kLmPassTiles) * kLmTile * 4; e += kLmThreads) {
+                    for (int e = tid; e < (HT + PT) * kLmTile * 4; e += kLmThreads) {
                         const int row = e >> 2;
                         *reinterpret_cast<uint4*>(stage[st] + row * (CH * 16) +
                                                   swz<CH>(row & 15, 4 + (e & 3)) * 16) = make_uint4(0, 0, 0, 0);
@@ -491,31 +502,41 @@ void lmhead_argmax(LArgs a, const uint16_t* __restrict__ hid, const uint16_t* __
     wait_vmcnt<0>();
 }
 
-template <int MT>
+template <int MT, int NT>
 void launch_lmhead(const LArgs& a, const uint16_t* hid, const uint16_t* wt, uint64_t* partial,
                    hipStream_t stream) {
-    hipLaunchKernelGGL(lmhead_argmax<MT>, dim3(a.nwg), dim3(kLmThreads), 0, stream, a, hid, wt,
-                       partial);
+    hipLaunchKernelGGL((lmhead_argmax<MT, NT>), dim3(a.nwg), dim3(kLmThreads), 0, stream, a, hid,
+                       wt, partial);
 }
 
-// launch lmhead_argmax<mt> (1 <= mt <= kLmMaxRT)
+// launch lmhead_argmax<mt, nt> (1 <= mt <= kLmMaxRT; nt kLmNT, or kLmNT + 1
+// where lm_wide_ok(mt))
 template <int M = 1>
-bool launch_lmhead_mt(int mt, const LArgs& a, const uint16_t* hid, const uint16_t* wt,
+bool launch_lmhead_mt(int mt, int nt, const LArgs& a, const uint16_t* hid, const uint16_t* wt,
                       uint64_t* partial, hipStream_t stream) {
     if constexpr (M > kLmMaxRT) {
         return false;
     } else {
         if (mt == M) {
-            launch_lmhead<M>(a, hid, wt, partial, stream);
-            return true;
+            if (nt == kLmNT) {
+                launch_lmhead<M, kLmNT>(a, hid, wt, partial, stream);
+                return true;
+            }
+            if constexpr (lm_wide_ok(M)) {
+                if (nt == kLmNT + 1) {
+                    launch_lmhead<M, kLmNT + 1>(a, hid, wt, partial, stream);
+                    return true;
+                }
+            }
+            return false;
         }
-        return launch_lmhead_mt<M + 1>(mt, a, hid, wt, partial, stream);
+        return launch_lmhead_mt<M + 1>(mt, nt, a, hid, wt, partial, stream);
     }
 }
 
 struct LmPlan {
     LArgs a;
-    int mt;
+    int mt, nt;
     size_t partial_bytes, argmax_bytes;
 };
 
@@ -560,6 +581,12 @@ LmPlan plan_lmhead(int32_t total_q, int32_t hidden_size, int64_t vocab) {
     a.ncols = a.xg * ((a.kg + a.nc - 1) / a.nc);
     const int htc = (rows_max + kLmTile - 1) / kLmTile;
     pl.mt = std::max(1, (htc + kLmRowGroups - 1) / kLmRowGroups);
+    // vocabulary tiles per wavefront and pass: the fewest tile slots for the
+    // largest workgroup's tiles (ties to the narrower)
+    const int64_t per_group = (a.tiles + a.xg - 1) / a.xg;
+    const int64_t ntw = (per_group + a.kg / a.nc - 1) / (a.kg / a.nc);
+    auto slots = [&](int nt) { return (ntw + kLmVocGroups * nt - 1) / (kLmVocGroups * nt) * nt; };
+    pl.nt = lm_wide_ok(pl.mt) && slots(kLmNT + 1) < slots(kLmNT) ? kLmNT + 1 : kLmNT;
     a.nk = (hidden_size + kLmStep - 1) / kLmStep;
     a.tail = hidden_size % kLmStep != 0;
     pl.partial_bytes = align_up((size_t)total_q * a.ncols * sizeof(uint64_t), 256);
@@ -605,7 +632,7 @@ extern "C" int verify_lmhead_accept(int32_t num_seqs, int32_t total_q, int32_t h
     if (total_q > 0) {
         const uint16_t* hs = static_cast<const uint16_t*>(hidden);
         const uint16_t* ws = static_cast<const uint16_t*>(weight);
-        if (!launch_lmhead_mt(pl.mt, pl.a, hs, ws, partial, stream)) return VERIFY_EUNSUPPORTED;
+        if (!launch_lmhead_mt(pl.mt, pl.nt, pl.a, hs, ws, partial, stream)) return VERIFY_EUNSUPPORTED;
         if (check_launch() != VERIFY_OK) return VERIFY_EHIP;
     }
     return launch_accept_scan(num_seqs, q_start, tokens, partial, pl.a.ncols, am, accept_len,

@@ -100,6 +100,8 @@ CASES = [
                                          # workgroups per XCD group (a column left neutral)
     ([7] * 111, 64, 777),                # 777 rows, 49 tiles: one group of 49 workgroups, 3 chunks
     ([33] * 300, 64, 4096),              # 9900 rows: two rounds of 32 chunks
+    ([9] * 20, 64, 90001),               # 180 rows, 22 tiles per workgroup: six vocabulary
+                                         # tiles per wavefront (one pass, not two of five)
     ([3, 8, 1], 2880, 4099),
 ]
 
