@@ -325,7 +325,8 @@ struct MPtrs {
     const int32_t* q_start;
     uint16_t* out;
     int32_t* unit_start;  // [num_seqs + 1] first unit of each request (schedule pass)
-    float* slot_o;        // [slots][rows_per_group][D] normalised partial outputs (slot_o_index)
+    uint16_t* slot_o;     // [slots][rows_per_group][D] normalised partial outputs, bf16
+                          // (slot_o_index)
     float* slot_lse;      // [slots][rows_per_group]    their log2-sum-exp
 };
 
@@ -336,7 +337,11 @@ struct ReqGeom {
 // Offset in slot_o of row lr (within the row group), dims d .. d+3 (d % 4 ==
 // 0), of slot `slot`.  Each 16-row tile of a slot is stored in the order the
 // MFMA output registers hold it: 16-dim column block dt, then lane
-// 16 (d / 4 % 4) + lr % 16, then the four dims.
+// 16 (d / 4 % 4) + lr % 16, then the four dims.  The partial outputs are
+// stored in bf16 (the log2-sum-exp in fp32), as a split-K merge usually keeps
+// them in the output's type: they are normalised, so rounding them adds at most
+// 2^-9 relative error to the merged row, and it halves the bytes written at
+// the end of every range and read back by the merge.
 template <int D>
 __device__ __forceinline__ int64_t slot_o_index(int64_t slot, int rows_per_group, int lr, int d) {
     const int lane = ((d >> 2) & 3) * 16 + (lr & 15);
@@ -596,7 +601,7 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     const uint8_t* __restrict__ vcg, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
     int32_t* __restrict__ unit_start, uint16_t* __restrict__ out,
-    float* __restrict__ slot_o, float* __restrict__ slot_lse) {
+    uint16_t* __restrict__ slot_o, float* __restrict__ slot_lse) {
     constexpr int NT = NW * kWave;
     constexpr int TILE_BYTES = kBlockTokens * D * 2;  // one (block, head) K or V tile
     constexpr int CH = 2 * TILE_BYTES / 16;           // 16-byte chunks per block (K then V)
@@ -740,14 +745,16 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
                     *reinterpret_cast<uint2*>(out + hrow * D + d0) = v;
                 }
             } else {
-                // the tile's 16 rows x D floats in register order (see
-                // slot_o_index): each store writes 1 KiB contiguous
+                // the tile's 16 rows x D values in register order (see
+                // slot_o_index): each store writes 512 bytes contiguous
                 const float inv = L > 0.f ? 1.f / L : 0.f;
                 const int64_t srow = slot * ROWS + lr;
-                float* tb = slot_o + (slot * ROWS + (wv * TPW + t) * 16) * D + lane * 4;
+                uint16_t* tb = slot_o + (slot * ROWS + (wv * TPW + t) * 16) * D + lane * 4;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt)
-                    *reinterpret_cast<f32x4_t*>(tb + dt * (kWave * 4)) = o[t][dt] * inv;
+                    *reinterpret_cast<uint2*>(tb + dt * (kWave * 4)) =
+                        make_uint2(pack_bf16x2(o[t][dt][0] * inv, o[t][dt][1] * inv),
+                                   pack_bf16x2(o[t][dt][2] * inv, o[t][dt][3] * inv));
                 if (lg == 0) slot_lse[srow] = L > 0.f ? m_r[t] + log2f(L) : -INFINITY;
             }
         }
@@ -843,7 +850,7 @@ constexpr int kCombineSlots = 8;
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
     PArgs a, const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
-    const int32_t* __restrict__ unit_start, const float* __restrict__ slot_o,
+    const int32_t* __restrict__ unit_start, const uint16_t* __restrict__ slot_o,
     const float* __restrict__ slot_lse, uint16_t* __restrict__ out) {
     constexpr int QUADS = D / 4;                       // 4-dim vectors per row
     constexpr int RPB = kCombineThreads / QUADS;       // rows per workgroup
@@ -884,9 +891,10 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
                 const int64_t srow = (slot0 + s0 + k) * ROWS + lr;
                 const bool in = s0 + k < ns;
                 lse[k] = in ? slot_lse[srow] : -INFINITY;
-                o[k] = in ? *reinterpret_cast<const f32x4_t*>(
-                                slot_o + slot_o_index<D>(slot0 + s0 + k, ROWS, lr, d0))
-                          : f32x4_t{0.f, 0.f, 0.f, 0.f};
+                const uint2 v = in ? *reinterpret_cast<const uint2*>(
+                                         slot_o + slot_o_index<D>(slot0 + s0 + k, ROWS, lr, d0))
+                                   : make_uint2(0, 0);
+                o[k] = f32x4_t{bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y)};
             }
             float m = M;
 #pragma unroll
@@ -1210,7 +1218,7 @@ int plan_class(const verify_attn_params* p, int64_t rows, int64_t nb_max, int ro
     }
     c.slots = pairs + c.nwg;
     c.unit_bytes = align_up(sizeof(int32_t) * ((size_t)std::max(1, p->num_seqs) + 1), 256);
-    c.slot_o_bytes = align_up((size_t)c.slots * per * p->head_dim * sizeof(float), 256);
+    c.slot_o_bytes = align_up((size_t)c.slots * per * p->head_dim * sizeof(uint16_t), 256);
     c.slot_lse_bytes = align_up((size_t)c.slots * per * sizeof(float), 256);
     return VERIFY_OK;
 }
@@ -1381,7 +1389,7 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
             const AttnPlan::Class& c = pl.cls[k];
             char* ws = static_cast<char*>(workspace) + c.off;
             m.unit_start = reinterpret_cast<int32_t*>(ws);
-            m.slot_o = reinterpret_cast<float*>(ws + c.unit_bytes);
+            m.slot_o = reinterpret_cast<uint16_t*>(ws + c.unit_bytes);
             m.slot_lse = reinterpret_cast<float*>(ws + c.unit_bytes + c.slot_o_bytes);
             a.rows_per_group = c.nw * c.tpw * 16;
             a.rg_max = c.rg_max;
