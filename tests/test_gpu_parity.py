@@ -302,6 +302,26 @@ def test_attention_long_pairs(hq, hkv, d):
         _check_paged(p, split=split, what="long pairs split=%d" % split)
 
 
+@pytest.mark.parametrize("contexts", [[1500, 3100, 40, 1030, 900, 2000, 0, 1200],
+                                      [40, 300, 77, 5, 200, 130, 0, 60]])
+def test_attention_row_classes(contexts):
+    """A ragged batch at head dim 128 whose largest request needs the
+    four-wavefront shape runs in two launches: requests with at most 48 rows
+    per KV head (12 rows at Hq/Hkv = 4, the boundary itself included) on the
+    three-tile shape (long contexts: one wavefront; short: two), the others on
+    the four-wavefront shape; every row of both against the oracle."""
+    say("attn row classes", contexts[:3])
+    drafts = [11, 12, 0, 32, 20, 3, 11, 40]   # 48 | 52 | 4 | 132 | 84 | 16 | 48 | 164 rows
+    p = random_paged(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype="bf16",
+                     contexts=contexts, drafts=drafts, seed=len(contexts) + contexts[0])
+    dv = _to_dev(p)
+    plan = av.attention_plan(dv["q"], dv["kc"], dv["bt"], max_q_len=int(np.diff(p.q_start).max()),
+                             max_seq_len=int(p.seq_lens.max()))
+    assert len(plan["classes"]) == 2 and plan["classes"][0]["rows_hi"] == 48
+    for split in (0, 1, 3):
+        _check_paged(p, split=split, what="row classes split=%d" % split)
+
+
 SEEDS = range(5)
 EVERY_PAIR = ["qwen3_8b", "dsk_distill_8b", "gpt_oss_20b"]
 
