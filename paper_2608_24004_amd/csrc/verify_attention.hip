@@ -859,6 +859,10 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
     const int i = P / per_req;
     const int rem = P - i * per_req;
     const int g = rem / a.rg_max, rg = rem - g * a.rg_max;
+    // the request's metadata and unit offsets are read together, before any
+    // test, so that they cost one memory latency instead of one each
+    const int U = unit_start[a.num_seqs];
+    const int ustart_i = unit_start[i];
     const ReqGeom rq = req_geom(a, q_start, seq_lens, i);
     if (rg >= rq.rg) return;
     const int ROWS = a.rows_per_group;
@@ -869,8 +873,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
     const bool empty = rq.nb == 0;
     int wf = 0, wl = 0;
     if (!empty) {
-        const int U = unit_start[a.num_seqs];
-        const int ps = unit_start[i] + (g * rq.rg + rg) * rq.nb;
+        const int ps = ustart_i + (g * rq.rg + rg) * rq.nb;
         wf = owner_of(a, ps, U);
         wl = owner_of(a, ps + rq.nb - 1, U);
         if (wf == wl) return;  // finished in place by its only workgroup
@@ -886,15 +889,23 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_slots(
         for (int s0 = 0; s0 < ns; s0 += kCombineSlots) {
             float lse[kCombineSlots];
             f32x4_t o[kCombineSlots];
+            // every load is issued unconditionally (slots past the pair's last
+            // re-read the last one and are masked afterwards), so that the
+            // round's loads leave back to back; conditional loads compiled to a
+            // branch and a wait per slot, one memory latency each
+            uint2 v[kCombineSlots];
 #pragma unroll
             for (int k = 0; k < kCombineSlots; ++k) {
-                const int64_t srow = (slot0 + s0 + k) * ROWS + lr;
+                const int64_t sl = slot0 + min(s0 + k, ns - 1);
+                lse[k] = slot_lse[sl * ROWS + lr];
+                v[k] = *reinterpret_cast<const uint2*>(slot_o + slot_o_index<D>(sl, ROWS, lr, d0));
+            }
+#pragma unroll
+            for (int k = 0; k < kCombineSlots; ++k) {
                 const bool in = s0 + k < ns;
-                lse[k] = in ? slot_lse[srow] : -INFINITY;
-                const uint2 v = in ? *reinterpret_cast<const uint2*>(
-                                         slot_o + slot_o_index<D>(slot0 + s0 + k, ROWS, lr, d0))
-                                   : make_uint2(0, 0);
-                o[k] = f32x4_t{bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y)};
+                lse[k] = in ? lse[k] : -INFINITY;
+                o[k] = in ? f32x4_t{bf16_lo(v[k].x), bf16_hi(v[k].x), bf16_lo(v[k].y), bf16_hi(v[k].y)}
+                          : f32x4_t{0.f, 0.f, 0.f, 0.f};
             }
             float m = M;
 #pragma unroll
