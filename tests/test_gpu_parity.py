@@ -291,6 +291,33 @@ def test_attention_batches_above_the_inline_schedule(dtype, hq, hkv, d):
         _check_paged(p, split=split, what="300 requests split=%d" % split)
 
 
+@pytest.mark.parametrize("window,with_sinks", [(0, False), (40, True)])
+def test_attention_batches_above_the_inline_schedule_in_row_classes(window, with_sinks):
+    # more than 256 requests with draft lengths on both sides of the row-class
+    # boundary: two launches, each with its own schedule launch and merge,
+    # with a sliding window and sinks in one case
+    rng = np.random.default_rng(301 + window)
+    B = 300
+    contexts = rng.integers(0, 200, size=B)
+    drafts = rng.integers(0, 21, size=B)
+    drafts[::37] = -1
+    say("attn 300 requests, row classes", window, with_sinks)
+    p = random_paged(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype="bf16",
+                     contexts=contexts.tolist(), drafts=drafts.tolist(), window=window, seed=7)
+    sinks = (rng.standard_normal(32) * 2.0).astype(np.float32) if with_sinks else None
+    d = _to_dev(p)
+    max_q_len = int(np.diff(p.q_start).max())
+    plan = av.attention_plan(d["q"], d["kc"], d["bt"], max_q_len=max_q_len,
+                             max_seq_len=int(p.seq_lens.max()), sliding_window=window)
+    assert len(plan["classes"]) == 2
+    ref = oracle.attention(sinks=None if sinks is None else sinks.astype(np.float64), **p.oracle_args())
+    for split in (0, 3):
+        out = gpu_attention(d["q"], d["kc"], d["vc"], d["bt"], d["sl"], d["qs"], max_q_len=max_q_len,
+                            max_seq_len=int(p.seq_lens.max()), window=window, split=split,
+                            sinks=None if sinks is None else torch.as_tensor(sinks, device=DEV))
+        assert_attention_close(to_host_f64(out), ref, "bf16", "300 requests row classes split=%d" % split)
+
+
 @pytest.mark.parametrize("hq,hkv,d", [(64, 8, 64), (32, 8, 128), (16, 2, 64)])
 def test_attention_long_pairs(hq, hkv, d):
     # pairs of 64 blocks and more run on the one-wavefront shapes (72 rows at
