@@ -8,6 +8,7 @@ import os
 import re
 
 import pytest
+import torch
 
 import paper_2608_24004_amd as av
 
@@ -322,3 +323,49 @@ def test_binding_checks_tensor_shapes_dtypes_and_devices():
         av.verify_kv_append(torch.empty(36, 8, 128, dtype=bf, **m), torch.empty(36, 8, 64, dtype=bf, **m),
                             base["k_cache"], base["v_cache"], base["block_tables"], base["seq_lens"],
                             base["q_start"])
+
+
+def _plan(p, total_q, max_q, max_s):
+    info = (ctypes.c_int32 * av.PLAN_INFO)()
+    assert av.library().verify_attention_plan(ctypes.byref(p), total_q, max_q, max_s, info) == 0
+    return [int(x) for x in info]
+
+
+def test_attention_plan_row_classes():
+    """The host side of the bf16 schedule (no GPU needed: without one the
+    library assumes 256 compute units and two resident workgroups each)."""
+    # Qwen-shaped: 36 rows per KV head, long contexts -> one launch, the
+    # one-wavefront three-tile shape (48 rows per group), one row group
+    q = _plan(_params(num_seqs=32, max_blocks_per_seq=1026), 288, 9, 16393)
+    assert q[0] == 1 and q[5] == 1 and q[2] == 48 and q[3] == 1 and q[10] == 2 ** 31 - 1
+    # ragged drafts up to 32 (132 rows): two launches, requests of up to 48
+    # rows on the three-tile shape, the rest on the four-wavefront shape
+    # (128 rows per group, two row groups)
+    r = _plan(_params(num_seqs=32, max_blocks_per_seq=1026), 500, 33, 16393)
+    assert r[5] == 2 and r[10] == 48
+    assert r[2] == 48 and r[3] == 1 and r[7] == 128 and r[8] == 2
+    # short contexts (fewer than 64 blocks): the first class takes the
+    # two-wavefront two-tile shape instead
+    s = _plan(_params(num_seqs=32, max_blocks_per_seq=64), 500, 33, 900)
+    assert s[5] == 2 and s[2] == 64 and s[7] == 128
+    # the long-context batch (8195 blocks at most): its classes own up to
+    # 128 * 8 * 8195 and twice that many units, 4 and 8 times 4096 per
+    # resident workgroup (512), so they launch 4 and 8 times as many
+    lc = _plan(_params(num_seqs=128, max_blocks_per_seq=8196), 2200, 33, 131105)
+    assert lc[5] == 2 and lc[1] == 4 * 512 and lc[6] == 8 * 512
+    # the Qwen-shaped batch stays at the resident count
+    assert q[1] == 512
+    # at most 12 rows per KV head with G = 4 stays one launch; 20 rows at
+    # G = 4 (five tiles) splits
+    assert _plan(_params(num_seqs=8, max_blocks_per_seq=1026), 100, 12, 16393)[5] == 1
+    assert _plan(_params(num_seqs=8, max_blocks_per_seq=1026), 100, 20, 16393)[5] == 2
+    # head dim 64 keeps one launch at any draft length
+    d64 = _plan(_params(num_seqs=8, num_q_heads=64, head_dim=64, max_blocks_per_seq=1026), 300, 33, 16393)
+    assert d64[5] == 1
+    # the binding reports the classes with their row bounds
+    qt = torch.zeros(500, 32, 128, dtype=torch.bfloat16)
+    kc = torch.zeros(40, 8, 16, 16, 8, dtype=torch.bfloat16)
+    bt = torch.zeros(32, 1026, dtype=torch.int32)
+    plan = av.attention_plan(qt, kc, bt, max_q_len=33, max_seq_len=16393)
+    assert [c["rows_lo"] for c in plan["classes"]] == [0, 49]
+    assert plan["classes"][0]["rows_hi"] == 48 and plan["rows_per_group"] == 48
