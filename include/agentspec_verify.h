@@ -360,6 +360,57 @@ int verify_budget(int32_t num_seqs, int32_t num_cands, int32_t max_cand_len,
                   int32_t *draft_len, int32_t *q_start, int32_t *tokens, int64_t tokens_capacity,
                   int32_t *seq_lens, hipStream_t stream);
 
+/*
+ * verify_check_batch -- validation of a verify batch's descriptor on the
+ * device, for callers that want bad data reported rather than given the
+ * defined behaviour of the calls above (which skip block ids outside the
+ * cache, write zeros for rows without visible keys and NaN for rows a launch
+ * does not reach, and may read out of bounds if q_start does not describe
+ * total_q rows).  It checks the preconditions of the packed-request
+ * convention (Sec. 2.2 scoring of n_i = k_i + 1 positions per request) and of
+ * verify_attention / verify_kv_append.  Nothing else is read or written.
+ *
+ *   num_seqs, total_q, q_start   as for verify_attention and verify_accept
+ *   max_q_len    > 0: the host bound on n_i to check; 0: not checked
+ *   params       NULL: only q_start (and max_q_len) are checked, as the
+ *                acceptance calls use it.  Otherwise the attention layer's
+ *                shape (num_seqs must agree; block_size 16), and:
+ *   max_seq_len  host bound on S_i
+ *   seq_lens     [num_seqs] int32, required with params
+ *   block_tables [num_seqs][max_blocks_per_seq] int32 or NULL (ids unchecked)
+ *   counts       int32[VERIFY_CHECK_COUNTS] on the device, reset and written
+ *                by the call (asynchronously, on `stream`):
+ *     [VERIFY_CHECK_ROWS]     requests i whose q_start[i] < 0,
+ *                             q_start[i + 1] < q_start[i] or > total_q, with
+ *                             q_start[0] != 0 or q_start[num_seqs] != total_q
+ *                             counted against the first or last request
+ *     [VERIFY_CHECK_QLEN]     requests with n_i > max_q_len
+ *     [VERIFY_CHECK_SHORT]    requests with S_i < n_i (rows without keys)
+ *     [VERIFY_CHECK_LONG]     requests with S_i > max_seq_len or
+ *                             S_i > 16 * max_blocks_per_seq
+ *     [VERIFY_CHECK_BLOCK_ID] requests with a block id outside
+ *                             [0, num_blocks) among the blocks their rows can
+ *                             read: positions [lo, min(S_i, 16 *
+ *                             max_blocks_per_seq)), lo = 0 without a window,
+ *                             else max(0, S_i - n_i - W + 1)
+ *     [VERIFY_CHECK_FIRST]    the lowest offending request, INT32_MAX if none
+ * VERIFY_EINVAL (nothing enqueued) on negative sizes, a NULL counts, a NULL
+ * q_start with num_seqs > 0, seq_lens or block_tables without params, or
+ * params that disagree with num_seqs.  The index arrays are read only within
+ * their stated sizes, whatever they hold.
+ */
+#define VERIFY_CHECK_ROWS 0
+#define VERIFY_CHECK_QLEN 1
+#define VERIFY_CHECK_SHORT 2
+#define VERIFY_CHECK_LONG 3
+#define VERIFY_CHECK_BLOCK_ID 4
+#define VERIFY_CHECK_FIRST 5
+#define VERIFY_CHECK_COUNTS 6
+int verify_check_batch(int32_t num_seqs, int32_t total_q, int32_t max_q_len,
+                       const int32_t *q_start, const verify_attn_params *params,
+                       int32_t max_seq_len, const int32_t *seq_lens,
+                       const int32_t *block_tables, int32_t *counts, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char *verify_status_string(int status);
 

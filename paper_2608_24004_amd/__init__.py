@@ -10,6 +10,9 @@ If the library is missing, every entry point raises -- there is no fallback.
     verify_lmhead_accept(...)  the same acceptance fed by the LM head, logits
                                never stored
     verify_accept_sampled(...), verify_budget(...), verify_kv_append(...)
+    check_batch(...)           the batch descriptor's preconditions, checked on
+                               the device (the calls above take ``check=True``,
+                               or every call does with AGENTSPEC_VERIFY_CHECK=1)
 """
 from __future__ import annotations
 
@@ -23,17 +26,34 @@ __all__ = ["verify_attention", "verify_accept", "verify_accept_noalloc", "verify
            "verify_lmhead_accept",
            "verify_budget", "verify_kv_append", "attention_workspace_size", "attention_plan",
            "accept_workspace_size",
-           "lmhead_accept_workspace_size", "VerifyError", "library", "abi_version", "F32", "BF16"]
+           "lmhead_accept_workspace_size", "check_batch", "BatchError", "VerifyError", "library",
+           "abi_version", "F32", "BF16"]
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
 NOALLOC_SCRATCH_BYTES = 4 << 20  # VERIFY_NOALLOC_SCRATCH_BYTES of the C header
 F32, BF16 = 0, 1
+# verify_check_batch's counts, in the order of VERIFY_CHECK_ROWS .. _BLOCK_ID,
+# then the first offending request (VERIFY_CHECK_FIRST)
+CHECK_KINDS = ("rows", "q_len", "short_seq", "long_seq", "block_id")
+CHECK_COUNTS = 6
+CHECK_BY_DEFAULT = os.environ.get("AGENTSPEC_VERIFY_CHECK", "0") == "1"
 
 
 class VerifyError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
         super().__init__("%s: %s (status %d)" % (where, _status_string(status), status))
+
+
+class BatchError(ValueError):
+    """A batch descriptor that fails verify_check_batch: ``counts`` maps each
+    kind in CHECK_KINDS to its number of offending requests, ``first`` is the
+    lowest offending request."""
+
+    def __init__(self, where: str, counts: dict, first: int):
+        self.counts, self.first = counts, first
+        bad = ", ".join("%s %d" % (k, v) for k, v in counts.items() if v)
+        super().__init__("%s: bad batch descriptor (%s; first request %d)" % (where, bad, first))
 
 
 class AttnParams(ctypes.Structure):
@@ -93,6 +113,8 @@ def library(path: Optional[str] = None):
     lib.verify_budget.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, f64, f64, vp, vp, vp, vp, vp, vp,
                                   vp, i64, vp, vp]
     lib.verify_budget.restype = ctypes.c_int
+    lib.verify_check_batch.argtypes = [i32, i32, i32, vp, P, i32, vp, vp, vp, vp]
+    lib.verify_check_batch.restype = ctypes.c_int
     lib.verify_status_string.argtypes = [ctypes.c_int]
     lib.verify_status_string.restype = ctypes.c_char_p
     lib.verify_abi_version.argtypes = []
@@ -208,6 +230,60 @@ def _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_block
     return params
 
 
+def check_batch(q_start, total_q: int, *, max_q_len: int = 0, seq_lens=None, block_tables=None,
+                num_blocks: int = 0, max_seq_len: int = 0, sliding_window: int = 0, stream=None):
+    """The batch descriptor's preconditions, checked on the device by
+    verify_check_batch.  Waits for the call's stream and returns (counts,
+    first): offending requests per kind of CHECK_KINDS, and the lowest
+    offending request (-1 if none).
+
+    Only q_start (and n_i <= max_q_len when max_q_len > 0) is checked unless
+    seq_lens is given; then also n_i <= S_i <= max_seq_len, and with
+    block_tables and num_blocks the ids of every block the rows can read
+    (keys from the first row's window start, sliding_window > 0, or 0)."""
+    import torch
+    i32 = torch.int32
+    if q_start.dim() != 1 or q_start.shape[0] < 1:
+        raise ValueError("q_start must be [B + 1], got %s" % (tuple(q_start.shape),))
+    B = q_start.shape[0] - 1
+    dev = q_start.device
+    params = None
+    if seq_lens is not None:
+        _expect(seq_lens, "seq_lens", (B,), i32, dev)
+        params = AttnParams(num_seqs=B, block_size=16, num_blocks=int(num_blocks),
+                            sliding_window=int(sliding_window),
+                            max_blocks_per_seq=(1 << 31) // 16 - 1)
+        if block_tables is not None:
+            if block_tables.dim() != 2 or block_tables.shape[0] != B or block_tables.shape[1] < 1:
+                raise ValueError("block_tables must be [B, max_blocks], got %s"
+                                 % (tuple(block_tables.shape),))
+            _expect(block_tables, "block_tables", None, i32, dev)
+            params.max_blocks_per_seq = block_tables.shape[1]
+    elif block_tables is not None:
+        raise ValueError("block_tables are checked against seq_lens, which is missing")
+    counts = torch.empty(CHECK_COUNTS, dtype=i32, device=dev)
+    rc = library().verify_check_batch(
+        B, int(total_q), int(max_q_len), _dev_ptr(q_start, "q_start", i32),
+        ctypes.byref(params) if params is not None else None, int(max_seq_len),
+        _dev_ptr(seq_lens, "seq_lens", i32), _dev_ptr(block_tables, "block_tables", i32),
+        _dev_ptr(counts, "counts", i32), _stream_ptr(stream, dev))
+    _check(rc, "verify_check_batch")
+    (stream if stream is not None else torch.cuda.current_stream(dev)).synchronize()
+    c = counts.cpu().tolist()
+    return dict(zip(CHECK_KINDS, c[:len(CHECK_KINDS)])), (c[-1] if c[-1] != 2 ** 31 - 1 else -1)
+
+
+def _checked(check, where, **kw):
+    """Raise BatchError before `where` launches anything if the descriptor
+    fails verify_check_batch (with check=True, or by default when
+    AGENTSPEC_VERIFY_CHECK=1)."""
+    if not (CHECK_BY_DEFAULT if check is None else check):
+        return
+    counts, first = check_batch(**kw)
+    if any(counts.values()):
+        raise BatchError(where, counts, first)
+
+
 def attention_workspace_size(q, k_cache, block_tables, *, max_q_len: int, max_seq_len: int,
                              sliding_window: int = 0, scale: float = 0.0,
                              kv_split_blocks: int = 0) -> int:
@@ -243,18 +319,23 @@ def attention_plan(q, k_cache, block_tables, *, max_q_len: int, max_seq_len: int
 def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, max_q_len: int,
                      max_seq_len: int, sliding_window: int = 0, scale: float = 0.0,
                      kv_split_blocks: int = 0, sinks=None, out=None, workspace=None,
-                     stream=None):
+                     stream=None, check=None):
     """Attention of every packed query row against its request's paged KV cache.
 
     q [T, Hq, D]; k_cache [NB, Hkv, D/x, 16, x]; v_cache [NB, Hkv, D, 16] (bf16 or
     fp32, x = 16 bytes / element); block_tables [B, MB], seq_lens [B], q_start
     [B+1] int32 on the device.  max_q_len / max_seq_len are host upper bounds of
     n_i = q_start[i+1]-q_start[i] and S_i = seq_lens[i].  sinks: optional [Hq]
-    float32 device tensor of per-head sink logits.  Returns `out`.
+    float32 device tensor of per-head sink logits.  Returns `out`.  check:
+    validate the descriptor on the device first (check_batch; raises
+    BatchError, waits for the stream).
     """
     import torch
     _check_attention_tensors(q, k_cache, v_cache, block_tables, seq_lens, q_start, sinks, out,
                              workspace)
+    _checked(check, "verify_attention", q_start=q_start, total_q=q.shape[0], max_q_len=max_q_len,
+             seq_lens=seq_lens, block_tables=block_tables, num_blocks=k_cache.shape[0],
+             max_seq_len=max_seq_len, sliding_window=sliding_window, stream=stream)
     params = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
     if out is None:
         out = torch.empty_like(q)
@@ -319,17 +400,19 @@ def _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitte
 
 
 def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, num_emitted=None,
-                  emitted=None, workspace=None, stream=None):
+                  emitted=None, workspace=None, stream=None, check=None):
     """Vocabulary argmax of every row and greedy acceptance of the drafts.
 
     logits [T, V] (bf16 or fp32), tokens [T] and q_start [B+1] int32 on the
     device.  Returns (accept_len [B], num_emitted [B], emitted [T], argmax [T]).
+    check: validate q_start on the device first (check_batch).
     """
     import torch
     i32 = torch.int32
     B, T, V, code, argmax_out, accept_len, num_emitted, emitted, workspace, ws_have = \
         _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, workspace)
     _expect(tokens, "tokens", (T,), i32, logits.device)
+    _checked(check, "verify_accept", q_start=q_start, total_q=T, stream=stream)
     rc = library().verify_accept(
         B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
         _dev_ptr(q_start, "q_start", i32), _dev_ptr(argmax_out, "argmax_out", i32),
@@ -341,7 +424,7 @@ def verify_accept(logits, tokens, q_start, *, argmax_out=None, accept_len=None, 
 
 
 def verify_accept_noalloc(logits, tokens, q_start, *, argmax_out=None, accept_len=None,
-                          num_emitted=None, emitted=None, stream=None):
+                          num_emitted=None, emitted=None, stream=None, check=None):
     """verify_accept without a workspace: the library's per-GPU scratch array
     holds the partial maxima (for callers that cannot allocate; calls that
     overlap on one GPU race).  Outputs not passed in are allocated here, by
@@ -353,6 +436,7 @@ def verify_accept_noalloc(logits, tokens, q_start, *, argmax_out=None, accept_le
         _accept_buffers(logits, q_start, argmax_out, accept_len, num_emitted, emitted, None,
                         need_workspace=False)
     _expect(tokens, "tokens", (T,), i32, logits.device)
+    _checked(check, "verify_accept_noalloc", q_start=q_start, total_q=T, stream=stream)
     rc = library().verify_accept_noalloc(
         B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
         _dev_ptr(q_start, "q_start", i32), _dev_ptr(argmax_out, "argmax_out", i32),
@@ -364,7 +448,7 @@ def verify_accept_noalloc(logits, tokens, q_start, *, argmax_out=None, accept_le
 
 def verify_accept_sampled(logits, tokens, q_start, *, temperature: float, seed: int, offset: int = 0,
                           sampled_out=None, accept_len=None, num_emitted=None, emitted=None,
-                          workspace=None, stream=None):
+                          workspace=None, stream=None, check=None):
     """Stochastic verification at temperature T > 0: every row draws
     y ~ softmax(logits / T) (Gumbel-max with Philox4x32-10 noise keyed by
     `seed`, counter (v / 4, row, offset, 0)) and a request accepts its drafts
@@ -380,6 +464,7 @@ def verify_accept_sampled(logits, tokens, q_start, *, temperature: float, seed: 
     B, T, V, code, sampled_out, accept_len, num_emitted, emitted, workspace, ws_have = \
         _accept_buffers(logits, q_start, sampled_out, accept_len, num_emitted, emitted, workspace)
     _expect(tokens, "tokens", (T,), i32, logits.device)
+    _checked(check, "verify_accept_sampled", q_start=q_start, total_q=T, stream=stream)
     rc = library().verify_accept_sampled(
         B, T, V, V, code, _dev_ptr(logits, "logits"), _dev_ptr(tokens, "tokens", i32),
         _dev_ptr(q_start, "q_start", i32), float(temperature), int(seed), int(offset),
@@ -400,7 +485,7 @@ def lmhead_accept_workspace_size(num_seqs: int, total_q: int, hidden_size: int, 
 
 
 def verify_lmhead_accept(hidden, weight, tokens, q_start, *, argmax_out=None, accept_len=None,
-                         num_emitted=None, emitted=None, workspace=None, stream=None):
+                         num_emitted=None, emitted=None, workspace=None, stream=None, check=None):
     """LM head fused with greedy acceptance: logits <hidden[r], weight[v]> are
     reduced to each row's argmax inside the kernel (never stored), then the
     drafts are accepted as in verify_accept.
@@ -430,6 +515,7 @@ def verify_lmhead_accept(hidden, weight, tokens, q_start, *, argmax_out=None, ac
             _expect(t, name, (n,), i32, dev)
     if workspace is not None:
         _expect(workspace, "workspace", None, None, dev)
+    _checked(check, "verify_lmhead_accept", q_start=q_start, total_q=T, stream=stream)
     code = _dtype_code(hidden)
     if argmax_out is None:
         argmax_out = torch.empty(T, dtype=i32, device=dev)
@@ -505,9 +591,11 @@ def verify_budget(cand_start, cand_len, cand_tokens, last_token, *, alpha: float
 
 
 def verify_kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, q_start, *,
-                     stream=None):
+                     stream=None, check=None):
     """Write the new tokens' K/V ([T, Hkv, D], the cache's dtype) into their
-    paged-cache slots (position S_i - n_i + j for row j of request i), in place."""
+    paged-cache slots (position S_i - n_i + j for row j of request i), in place.
+    check: validate the descriptor and the new tokens' block ids on the device
+    first (check_batch with a one-key window: only those blocks)."""
     import torch
     if k_new.dim() != 3:
         raise ValueError("k_new must be [T, Hkv, D], got %s" % (tuple(k_new.shape),))
@@ -520,6 +608,9 @@ def verify_kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, q_s
         raise ValueError("k_new has %d KV heads, the cache %d" % (k_new.shape[1], k_cache.shape[1]))
     params = _attn_params(probe, k_cache, block_tables, 0, 0.0, 0)
     i32 = torch.int32
+    _checked(check, "verify_kv_append", q_start=q_start, total_q=k_new.shape[0], seq_lens=seq_lens,
+             block_tables=block_tables, num_blocks=k_cache.shape[0],
+             max_seq_len=16 * block_tables.shape[1], sliding_window=1, stream=stream)
     rc = library().verify_kv_append(
         ctypes.byref(params), k_new.shape[0], _dev_ptr(k_new, "k_new"),
         _dev_ptr(v_new, "v_new", k_new.dtype), _dev_ptr(block_tables, "block_tables", i32),

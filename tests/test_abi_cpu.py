@@ -30,7 +30,8 @@ def test_header_declares_the_entry_points():
     for n in ("verify_attention", "verify_accept", "verify_accept_sampled", "verify_budget",
               "verify_kv_append", "verify_attention_workspace_size",
               "verify_accept_workspace_size", "verify_lmhead_accept", "verify_accept_noalloc",
-              "verify_lmhead_accept_workspace_size", "verify_status_string", "verify_abi_version"):
+              "verify_lmhead_accept_workspace_size", "verify_check_batch", "verify_status_string",
+              "verify_abi_version"):
         assert n in names
 
 
@@ -38,7 +39,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10600
+    assert av.abi_version() == 10700
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
@@ -264,6 +265,34 @@ def test_kv_append_argument_validation():
     assert lib.verify_kv_append(ctypes.byref(_params()), -1, d, d, d, d, d, d, d, None) == av.EINVAL
     # nothing to append: a no-op that needs no pointers
     assert lib.verify_kv_append(ctypes.byref(_params()), 0, *([None] * 7), None) == 0
+
+
+def test_check_batch_argument_validation():
+    """verify_check_batch refuses bad arguments before any device call."""
+    lib = av.library()
+    d = ctypes.c_void_p(0x1000)
+    P = ctypes.byref
+    ok = lambda **kw: _params(num_seqs=4, **kw)
+    # negative sizes, no counts, no q_start
+    assert lib.verify_check_batch(-1, 10, 0, d, None, 0, None, None, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, -1, 0, d, None, 0, None, None, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, -1, d, None, 0, None, None, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, None, 0, None, None, None, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, None, None, 0, None, None, d, None) == av.EINVAL
+    # seq_lens or block tables need the layer's shape
+    assert lib.verify_check_batch(4, 10, 0, d, None, 0, d, None, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, None, 0, None, d, d, None) == av.EINVAL
+    # params that disagree with the call, or without seq_lens
+    assert lib.verify_check_batch(4, 10, 0, d, P(_params(num_seqs=5)), 100, d, d, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, P(ok(block_size=32)), 100, d, d, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, P(ok(max_blocks_per_seq=0)), 100, d, d, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, P(ok(sliding_window=-1)), 100, d, d, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, P(ok()), -1, d, d, d, None) == av.EINVAL
+    assert lib.verify_check_batch(4, 10, 0, d, P(ok()), 100, None, d, d, None) == av.EINVAL
+    # the binding: block tables without seq_lens
+    qs = torch.zeros(5, dtype=torch.int32)
+    with pytest.raises(ValueError, match="seq_lens"):
+        av.check_batch(qs, 0, block_tables=torch.zeros((4, 2), dtype=torch.int32))
 
 
 def test_binding_checks_tensor_shapes_dtypes_and_devices():
