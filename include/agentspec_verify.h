@@ -22,6 +22,9 @@
  *                       step's q_start / tokens / seq_lens built from them.
  *   verify_kv_append -- the n_i new tokens' K/V written into their cache slots
  *                       before verify_attention reads them.
+ *   verify_attention_append -- both in one launch sequence: the attention
+ *                       reads the new tokens from the caller's arrays while it
+ *                       stores them into the cache.
  *   verify_accept_sampled -- verify_accept at a temperature T > 0: each row
  *                       draws its token from softmax(logits / T) instead of
  *                       taking the argmax (speculative sampling with drafts
@@ -30,8 +33,10 @@
  *                       logits of every scored position are computed from the
  *                       final hidden states and reduced to the argmax on the
  *                       fly, never stored.
+ *   verify_check_batch -- the batch descriptor's preconditions, checked on the
+ *                       device.
  *
- * Conventions shared by both calls
+ * Conventions shared by the calls
  * --------------------------------
  *  - Requests are packed: query rows q_start[i] .. q_start[i+1]-1 (int32,
  *    num_seqs+1 entries, q_start[0] = 0, non-decreasing) belong to request i;
@@ -141,6 +146,35 @@ int verify_attention(const verify_attn_params *params, int32_t total_q, int32_t 
                      const void *v_cache, const int32_t *block_tables,
                      const int32_t *seq_lens, const int32_t *q_start, const float *sinks,
                      void *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * verify_attention_append -- verify_kv_append and verify_attention in one
+ * launch sequence: the n_i new tokens' K/V of every request (the scored
+ * positions of Sec. 2.2 are the new tokens, positions S_i - n_i .. S_i - 1)
+ * are written into their cache slots, and the attention reads them from
+ * k_new / v_new while it walks the cache, so it never waits for the writes.
+ *
+ *   k_new, v_new [total_q][Hkv][D] (dtype): row j of request i holds the K
+ *                and V of position S_i - n_i + j (the layout of
+ *                verify_kv_append); required when total_q > 0
+ *   k_cache, v_cache: read as by verify_attention and written in place: every
+ *                new token whose position lies in [0, min(S_i, max_seq_len,
+ *                16 * max_blocks_per_seq)) and whose block id lies in
+ *                [0, num_blocks) is stored to its slot, element bits
+ *                unchanged; other new tokens are neither stored nor read.
+ *   all other arguments and the workspace as for verify_attention (the size
+ *   that verify_attention_workspace_size returns covers both calls).
+ * Under verify_attention's bounds (S_i <= max_seq_len <= 16 *
+ * max_blocks_per_seq), out and the cache equal, bit for bit, what
+ * verify_kv_append followed by verify_attention on the same stream writes.
+ * k_new / v_new must not overlap the caches.
+ */
+int verify_attention_append(const verify_attn_params *params, int32_t total_q, int32_t max_q_len,
+                            int32_t max_seq_len, const void *q, const void *k_new,
+                            const void *v_new, void *k_cache, void *v_cache,
+                            const int32_t *block_tables, const int32_t *seq_lens,
+                            const int32_t *q_start, const float *sinks, void *out,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * verify_attention_plan -- the work decomposition verify_attention would use

@@ -10,6 +10,7 @@ If the library is missing, every entry point raises -- there is no fallback.
     verify_lmhead_accept(...)  the same acceptance fed by the LM head, logits
                                never stored
     verify_accept_sampled(...), verify_budget(...), verify_kv_append(...)
+    verify_attention_append(...) the append and the attention in one launch
     check_batch(...)           the batch descriptor's preconditions, checked on
                                the device (the calls above take ``check=True``,
                                or every call does with AGENTSPEC_VERIFY_CHECK=1)
@@ -24,7 +25,8 @@ from .build import LIB_PATH
 
 __all__ = ["verify_attention", "verify_accept", "verify_accept_noalloc", "verify_accept_sampled",
            "verify_lmhead_accept",
-           "verify_budget", "verify_kv_append", "attention_workspace_size", "attention_plan",
+           "verify_budget", "verify_kv_append", "verify_attention_append",
+           "attention_workspace_size", "attention_plan",
            "accept_workspace_size",
            "lmhead_accept_workspace_size", "check_batch", "BatchError", "VerifyError", "library",
            "abi_version", "F32", "BF16"]
@@ -94,6 +96,9 @@ def library(path: Optional[str] = None):
     lib.verify_attention_plan.argtypes = [P, i32, i32, i32, ctypes.POINTER(i32)]
     lib.verify_attention_plan.restype = ctypes.c_int
     lib.verify_kv_append.argtypes = [P, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.verify_attention_append.argtypes = [P, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                            vp, sz, vp]
+    lib.verify_attention_append.restype = ctypes.c_int
     lib.verify_kv_append.restype = ctypes.c_int
     lib.verify_accept_workspace_size.argtypes = [i32, i32, i64, i32, ctypes.POINTER(sz)]
     lib.verify_accept_workspace_size.restype = ctypes.c_int
@@ -354,6 +359,46 @@ def verify_attention(q, k_cache, v_cache, block_tables, seq_lens, q_start, *, ma
         _dev_ptr(out, "out", q.dtype), _dev_ptr(workspace, "workspace"), ws_have,
         _stream_ptr(stream, q.device))
     _check(rc, "verify_attention")
+    return out
+
+
+def verify_attention_append(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, q_start, *,
+                            max_q_len: int, max_seq_len: int, sliding_window: int = 0,
+                            scale: float = 0.0, kv_split_blocks: int = 0, sinks=None, out=None,
+                            workspace=None, stream=None, check=None):
+    """verify_kv_append and verify_attention in one launch sequence: the new
+    tokens' K/V (k_new, v_new [T, Hkv, D], the cache's dtype) are stored into
+    k_cache / v_cache in place while the attention reads them from k_new /
+    v_new.  Same arguments and result as verify_attention; returns `out`."""
+    import torch
+    _check_attention_tensors(q, k_cache, v_cache, block_tables, seq_lens, q_start, sinks, out,
+                             workspace)
+    shape = (q.shape[0], k_cache.shape[1], q.shape[2])
+    _expect(k_new, "k_new", shape, q.dtype, q.device)
+    _expect(v_new, "v_new", shape, q.dtype, q.device)
+    _checked(check, "verify_attention_append", q_start=q_start, total_q=q.shape[0],
+             max_q_len=max_q_len, seq_lens=seq_lens, block_tables=block_tables,
+             num_blocks=k_cache.shape[0], max_seq_len=max_seq_len, sliding_window=sliding_window,
+             stream=stream)
+    params = _attn_params(q, k_cache, block_tables, sliding_window, scale, kv_split_blocks)
+    if out is None:
+        out = torch.empty_like(q)
+    ws_bytes = attention_workspace_size(q, k_cache, block_tables, max_q_len=max_q_len,
+                                        max_seq_len=max_seq_len, sliding_window=sliding_window,
+                                        scale=scale, kv_split_blocks=kv_split_blocks)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_have = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    i32 = torch.int32
+    rc = library().verify_attention_append(
+        ctypes.byref(params), q.shape[0], int(max_q_len), int(max_seq_len), _dev_ptr(q, "q"),
+        _dev_ptr(k_new, "k_new", q.dtype), _dev_ptr(v_new, "v_new", q.dtype),
+        _dev_ptr(k_cache, "k_cache", q.dtype), _dev_ptr(v_cache, "v_cache", q.dtype),
+        _dev_ptr(block_tables, "block_tables", i32), _dev_ptr(seq_lens, "seq_lens", i32),
+        _dev_ptr(q_start, "q_start", i32), _dev_ptr(sinks, "sinks", torch.float32),
+        _dev_ptr(out, "out", q.dtype), _dev_ptr(workspace, "workspace"), ws_have,
+        _stream_ptr(stream, q.device))
+    _check(rc, "verify_attention_append")
     return out
 
 

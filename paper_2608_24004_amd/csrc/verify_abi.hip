@@ -14,4 +14,4 @@ extern "C" const char* verify_status_string(int status) {
     }
 }
 
-extern "C" int verify_abi_version(void) { return 10700; }
+extern "C" int verify_abi_version(void) { return 10800; }

@@ -43,6 +43,8 @@ struct AttnArgs {
     float* part_o;    // [total_q][Hq][max_splits][D]   normalised partial outputs
     float* part_lse;  // [total_q][Hq][max_splits]      log2-sum-exp of each split
     const float* sinks;  // [Hq] sink logits (natural-log units) or null
+    const void* k_new;   // fused append: [total_q][Hkv][D] new keys and values, or null
+    const void* v_new;
     int num_seqs, hq, hkv, group, max_blocks, num_blocks, window, max_seq_len;
     float scale_log2;  // softmax scale * log2(e): scores live in the log2 domain
     int split_blocks, max_splits, row_groups;
@@ -59,6 +61,7 @@ __device__ __forceinline__ float sink_term(const float* sinks, int h, float m) {
 // Per-request geometry, recomputed identically by every kernel.
 struct SeqGeom {
     int q0, n, S, b_lo, b_hi, nsplit;
+    int s_raw;  // seq_lens[i] before clamping: the new tokens sit at s_raw - n .. s_raw - 1
 };
 
 __device__ __forceinline__ SeqGeom seq_geom(const AttnArgs& a, int i) {
@@ -66,6 +69,7 @@ __device__ __forceinline__ SeqGeom seq_geom(const AttnArgs& a, int i) {
     g.q0 = a.q_start[i];
     g.n = a.q_start[i + 1] - g.q0;
     int S = a.seq_lens[i];
+    g.s_raw = S;
     S = max(0, min(S, min(a.max_seq_len, a.max_blocks * kBlockTokens)));
     g.S = S;
     const int key_lo = a.window > 0 ? max(0, S - g.n - a.window + 1) : 0;
@@ -84,7 +88,11 @@ __device__ __forceinline__ SeqGeom seq_geom(const AttnArgs& a, int i) {
 //   output  lane owns D/64 consecutive output dimensions, reading V^T rows
 //           (16 keys of one dimension are contiguous in the V layout) and the
 //           16 probabilities of the block broadcast through readlane.
-template <typename T, int D>
+// APPEND: the fused KV append (verify_attention_append).  Keys and values of
+// the request's new tokens are read from k_new / v_new instead of the cache,
+// and the work items of row group 0 (splits cover disjoint blocks) store them
+// into the cache as well.
+template <typename T, int D, bool APPEND>
 __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
     constexpr int X = Storage<T>::kPer16B;  // elements per 16 bytes
     constexpr int NC = D / X;               // 16-byte chunks per key
@@ -146,16 +154,32 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
     const T* vc = static_cast<const T*>(a.vc);
     const int64_t tile = (int64_t)kBlockTokens * D;
     const int32_t* btab = a.block_tables + (int64_t)i * a.max_blocks;
+    // APPEND: new-token positions the walk reaches, and the first row's position
+    const int p0 = sg.s_raw - sg.n;
+    const int nlo = max(p0, 0), nhi = min(sg.s_raw, sg.S);
+    const T* knew = static_cast<const T*>(a.k_new);
+    const T* vnew = static_cast<const T*>(a.v_new);
 
     for (int b = sb + w; b < se; b += kAttnWaves) {
         const int phys = btab[b];
         if (phys < 0 || phys >= a.num_blocks) continue;
         const T* ktile = kc + ((int64_t)phys * a.hkv + kvh) * tile;
         const T* vtile = vc + ((int64_t)phys * a.hkv + kvh) * tile;
+        const int tk = b * kBlockTokens + t;
+        // APPEND: a new token's key comes from k_new (its row's 16-byte chunks)
+        const bool knew_t = APPEND && tk >= nlo && tk < nhi;
+        const int64_t nrow = (int64_t)sg.q0 + (tk - p0);
         float kf[CPL * X];
 #pragma unroll
-        for (int u = 0; u < CPL; ++u)
-            unpack16(ld16(ktile + ((dq * CPL + u) * kBlockTokens + t) * X), &kf[u * X], T());
+        for (int u = 0; u < CPL; ++u) {
+            const int c16 = dq * CPL + u;
+            const T* kp = knew_t ? knew + (nrow * a.hkv + kvh) * D + c16 * X
+                                 : ktile + (c16 * kBlockTokens + t) * X;
+            const uint4 kraw = ld16(kp);
+            if (APPEND && knew_t && rg == 0)
+                *reinterpret_cast<uint4*>(const_cast<T*>(ktile) + (c16 * kBlockTokens + t) * X) = kraw;
+            unpack16(kraw, &kf[u * X], T());
+        }
         float vf[DPL][kBlockTokens];
 #pragma unroll
         for (int e = 0; e < DPL; ++e) {
@@ -163,7 +187,23 @@ __global__ __launch_bounds__(kAttnThreads) void attn_valu(AttnArgs a) {
 #pragma unroll
             for (int c = 0; c < VCH; ++c) unpack16(ld16(vrow + c * X), &vf[e][c * X], T());
         }
-        const int tk = b * kBlockTokens + t;
+        if (APPEND && b * kBlockTokens < nhi && (b + 1) * kBlockTokens > nlo) {
+            // the new tokens' values: dimension lane * DPL + e of row
+            // q0 + (position - p0), for the block's new positions
+#pragma unroll
+            for (int tt = 0; tt < kBlockTokens; ++tt) {
+                const int pos = b * kBlockTokens + tt;
+                if (pos < nlo || pos >= nhi) continue;
+                const int64_t vrow_new = ((int64_t)sg.q0 + (pos - p0)) * a.hkv + kvh;
+#pragma unroll
+                for (int e = 0; e < DPL; ++e) {
+                    const int d = lane * DPL + e;
+                    const T v = vnew[vrow_new * D + d];
+                    vf[e][tt] = Storage<T>::load(&v, 0);
+                    if (rg == 0) const_cast<T*>(vtile)[d * kBlockTokens + tt] = v;
+                }
+            }
+        }
 
 #pragma unroll
         for (int r = 0; r < RB; ++r) {
@@ -328,6 +368,8 @@ struct MPtrs {
     uint16_t* slot_o;     // [slots][rows_per_group][D] normalised partial outputs, bf16
                           // (slot_o_index)
     float* slot_lse;      // [slots][rows_per_group]    their log2-sum-exp
+    const uint16_t* k_new;  // fused append: [total_q][Hkv][D] new keys, or null
+    const uint16_t* v_new;  //               and values
 };
 
 struct ReqGeom {
@@ -594,14 +636,22 @@ __device__ __forceinline__ bool block_needs_mask(int b, int p_first, int S, int 
 template <int TPW>
 constexpr int persist_waves_per_eu() { return TPW == 1 ? 4 : 2; }
 
-template <int D, int NW, int TPW, int PD>
+// APPEND: the fused KV append (verify_attention_append).  The request's new
+// tokens, positions S_i - n_i .. S_i - 1 of rows q_start[i] .. q_start[i+1]-1,
+// are taken from k_new / v_new: after a block holding some of them has landed
+// in LDS, the workgroup overwrites their K and V there (one extra barrier, on
+// those blocks only), and the workgroup of the pair's first row group also
+// stores them into the cache.  Readers never depend on that store, so no
+// ordering between workgroups is needed.
+template <int D, int NW, int TPW, int PD, bool APPEND>
 __global__ __launch_bounds__(NW * kWave)
 __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_persist(
     PArgs a, const uint16_t* __restrict__ qg, const uint8_t* __restrict__ kcg,
     const uint8_t* __restrict__ vcg, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
     int32_t* __restrict__ unit_start, uint16_t* __restrict__ out,
-    uint16_t* __restrict__ slot_o, float* __restrict__ slot_lse) {
+    uint16_t* __restrict__ slot_o, float* __restrict__ slot_lse,
+    const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new) {
     constexpr int NT = NW * kWave;
     constexpr int TILE_BYTES = kBlockTokens * D * 2;  // one (block, head) K or V tile
     constexpr int CH = 2 * TILE_BYTES / 16;           // 16-byte chunks per block (K then V)
@@ -680,6 +730,9 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
     // maximum, neg_m = -m_r (0 while the row has seen no key).
     float m_r[TPW], l_r[TPW], thr[TPW], neg_m[TPW];
     float sink_l2[TPW];  // the row's head's sink logit in the log2 domain (-inf: none)
+    // APPEND: the pair's new-token positions [st_nlo, st_nhi) (those the walk
+    // reaches) and the position of its first row, S_i - n_i
+    int st_nlo = 0, st_nhi = 0, st_p0 = 0;
 
     // Pair of cursor c, reached at unit u.
     auto init_pair = [&](const Cursor& c, int u) {
@@ -688,6 +741,12 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
         srq = c.rq;
         st_g = c.g;
         st_rg = c.r;
+        if constexpr (APPEND) {
+            const int s_raw = uniform_load(seq_lens + c.i);
+            st_p0 = s_raw - srq.n;
+            st_nlo = max(st_p0, 0);
+            st_nhi = min(s_raw, srq.S);
+        }
         const int rows = a.group * srq.n;
         const int wrow0 = st_rg * ROWS + wv * TPW * 16;
         active = wrow0 < rows;
@@ -793,6 +852,42 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
         }
     };
 
+    // APPEND: overwrite the new tokens of block b in stage st with their K and
+    // V from k_new / v_new (16 bytes = 8 dims of one token per step), and, in
+    // the pair's first row group, store them into the cache block as well.
+    auto patch_new = [&](int st, int b) {
+        constexpr int DC = D / 8;  // 16-byte chunks per key
+        const int pos0 = b * kBlockTokens;
+        const int t_lo = max(st_nlo - pos0, 0), t_hi = min(st_nhi - pos0, kBlockTokens);
+        uint8_t* ks = stage[st];
+        uint16_t* vs = reinterpret_cast<uint16_t*>(stage[st] + TILE_BYTES);
+        const bool writer = st_rg == 0;
+        const int phys = uniform_load(block_tables + (int64_t)st_i * a.max_blocks + b);
+        const int64_t toff = ((int64_t)phys * a.hkv + st_g) * TILE_BYTES;
+        uint8_t* kw = const_cast<uint8_t*>(kcg) + toff;
+        uint16_t* vw = reinterpret_cast<uint16_t*>(const_cast<uint8_t*>(vcg) + toff);
+        // K and V of one token's 8 dims per step, both loads in flight together
+        for (int e = tid; e < (t_hi - t_lo) * DC; e += NT) {
+            const int t = t_lo + e / DC, dc = e % DC;
+            const int64_t row = srq.q0 + (pos0 + t - st_p0);
+            const int64_t src = (row * a.hkv + st_g) * D + dc * 8;
+            const uint4 kv = ld16(k_new + src);
+            const uint4 vv = ld16(v_new + src);
+            const int kchunk = dc * kBlockTokens + t;
+            *reinterpret_cast<uint4*>(ks + kchunk * 16) = kv;
+            const uint32_t vh[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                vs[(dc * 8 + k) * kBlockTokens + t] = (uint16_t)(vh[k >> 1] >> (16 * (k & 1)));
+            if (writer) {
+                *reinterpret_cast<uint4*>(kw + kchunk * 16) = kv;
+#pragma unroll
+                for (int k = 0; k < 8; ++k)
+                    vw[(dc * 8 + k) * kBlockTokens + t] = (uint16_t)(vh[k >> 1] >> (16 * (k & 1)));
+            }
+        }
+    };
+
     // ---- pipeline: a ring of NS = PD + 1 LDS stages, PD blocks in flight.
     // At unit uu: wait for this thread's loads of uu (the PD - 1 younger units
     // may stay in flight), barrier (everyone's loads of uu have landed and
@@ -826,6 +921,14 @@ __attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_pers
         if (cc.i != st_i || cc.g != st_g || cc.r != st_rg) {
             flush_pair();
             init_pair(cc, uu);
+        }
+        if constexpr (APPEND) {
+            // block-uniform: every wavefront takes the same branch
+            const int pos0 = cc.b * kBlockTokens;
+            if (((ok_mask >> st) & 1u) && pos0 < st_nhi && pos0 + kBlockTokens > st_nlo) {
+                patch_new(st, cc.b);
+                lds_barrier();
+            }
         }
         compute(st, cc.b);
         asm volatile("" ::: "memory");
@@ -1125,9 +1228,9 @@ bool with_shape(int d, int nw, int tpw, F&& f) {
     return false;
 }
 
-template <typename S>
+template <typename S, bool APPEND = false>
 constexpr auto persist_kernel() {
-    return attn_persist<S::D, S::NW, S::TPW, S::PD>;
+    return attn_persist<S::D, S::NW, S::TPW, S::PD, APPEND>;
 }
 
 int validate(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
@@ -1161,14 +1264,14 @@ int device_cus() {
     return v;
 }
 
-template <typename S>
+template <typename S, bool APPEND = false>
 int resident_wgs() {
     static std::atomic<int> cache[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 2; }
     int v = cache[dev].load(std::memory_order_relaxed);
     if (v > 0) return v;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, persist_kernel<S>(), S::NW * kWave, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, persist_kernel<S, APPEND>(), S::NW * kWave, 0) !=
             hipSuccess ||
         v <= 0) {
         (void)hipGetLastError();
@@ -1206,7 +1309,7 @@ void pick_shape(int head_dim, int64_t tiles, int64_t nb_max, int& nw, int& tpw) 
 // The persistent launch of one row class: requests with rows_lo <= Hq/Hkv *
 // n_i <= rows_hi, of which no request has more than `rows` rows.
 int plan_class(const verify_attn_params* p, int64_t rows, int64_t nb_max, int rows_lo, int rows_hi,
-               AttnPlan::Class& c) {
+               bool append, AttnPlan::Class& c) {
     c = AttnPlan::Class{};
     pick_shape(p->head_dim, (rows + 15) / 16, nb_max, c.nw, c.tpw);
     c.rows_lo = rows_lo;
@@ -1221,7 +1324,11 @@ int plan_class(const verify_attn_params* p, int64_t rows, int64_t nb_max, int ro
         c.nwg = (int)std::min<int64_t>((units_max + c.spb - 1) / c.spb, (int64_t)1 << 30);
     } else {
         int res = 0;
-        if (!with_shape(p->head_dim, c.nw, c.tpw, [&](auto sh) { res = resident_wgs<decltype(sh)>(); }))
+        // the fused-append kernel holds more registers, and may fit fewer
+        // workgroups per compute unit
+        if (!with_shape(p->head_dim, c.nw, c.tpw, [&](auto sh) {
+                res = append ? resident_wgs<decltype(sh), true>() : resident_wgs<decltype(sh)>();
+            }))
             return VERIFY_EUNSUPPORTED;
         const int64_t resident = (int64_t)device_cus() * res;
         const int64_t mult = std::min<int64_t>(8, std::max<int64_t>(1, units_max / resident / kOversubUnits));
@@ -1235,7 +1342,7 @@ int plan_class(const verify_attn_params* p, int64_t rows, int64_t nb_max, int ro
 }
 
 int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
-              int32_t max_seq_len, AttnPlan* out) {
+              int32_t max_seq_len, AttnPlan* out, bool append = false) {
     AttnPlan pl{};
     const int G = p->num_q_heads / p->num_kv_heads;
     int64_t nb_max = ((int64_t)max_seq_len + kBlockTokens - 1) / kBlockTokens;
@@ -1257,12 +1364,12 @@ int make_plan(const verify_attn_params* p, int32_t total_q, int32_t max_q_len,
         int rc;
         if (p->head_dim == 128 && (rows + 15) / 16 >= 5) {
             pl.nclass = 2;
-            rc = plan_class(p, kShortClassRows, nb_max, 0, kShortClassRows, pl.cls[0]);
+            rc = plan_class(p, kShortClassRows, nb_max, 0, kShortClassRows, append, pl.cls[0]);
             if (rc == VERIFY_OK)
-                rc = plan_class(p, rows, nb_max, kShortClassRows + 1, INT32_MAX, pl.cls[1]);
+                rc = plan_class(p, rows, nb_max, kShortClassRows + 1, INT32_MAX, append, pl.cls[1]);
         } else {
             pl.nclass = 1;
-            rc = plan_class(p, rows, nb_max, 0, INT32_MAX, pl.cls[0]);
+            rc = plan_class(p, rows, nb_max, 0, INT32_MAX, append, pl.cls[0]);
         }
         if (rc != VERIFY_OK) return rc;
         size_t off = 0;
@@ -1306,9 +1413,14 @@ bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan::Class& pl, i
         if (!a.inline_sched)
             hipLaunchKernelGGL((attn_schedule<S::D>), dim3(1), dim3(1024), 0, stream, a, m.q_start,
                                m.seq_lens, m.unit_start, m.out);
-        hipLaunchKernelGGL(persist_kernel<S>(), dim3(a.nwg), dim3(S::NW * kWave), 0, stream, a, m.q,
-                           m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start, m.unit_start, m.out,
-                           m.slot_o, m.slot_lse);
+        if (m.k_new)
+            hipLaunchKernelGGL((persist_kernel<S, true>()), dim3(a.nwg), dim3(S::NW * kWave), 0, stream,
+                               a, m.q, m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start, m.unit_start,
+                               m.out, m.slot_o, m.slot_lse, m.k_new, m.v_new);
+        else
+            hipLaunchKernelGGL(persist_kernel<S>(), dim3(a.nwg), dim3(S::NW * kWave), 0, stream, a,
+                               m.q, m.kc, m.vc, m.block_tables, m.seq_lens, m.q_start, m.unit_start,
+                               m.out, m.slot_o, m.slot_lse, nullptr, nullptr);
         const int64_t pairs = (int64_t)a.num_seqs * a.hkv * a.rg_max;
         constexpr int RPB = kCombineThreads / (S::D / 4);
         // rows of a row group: at most rows_per_group, at most G * max_q_len
@@ -1324,7 +1436,10 @@ bool launch_persist(const PArgs& a, const MPtrs& m, const AttnPlan::Class& pl, i
 template <typename T, int D>
 void launch_valu(const AttnArgs& a, const AttnPlan& pl, int total_q, hipStream_t stream) {
     dim3 grid(pl.max_splits, a.hkv * pl.row_groups, a.num_seqs);
-    hipLaunchKernelGGL((attn_valu<T, D>), grid, dim3(kAttnThreads), 0, stream, a);
+    if (a.k_new)
+        hipLaunchKernelGGL((attn_valu<T, D, true>), grid, dim3(kAttnThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((attn_valu<T, D, false>), grid, dim3(kAttnThreads), 0, stream, a);
     const int64_t items = (int64_t)total_q * a.hq;
     if (items > 0) {
         dim3 cgrid((unsigned)((items + kAttnWaves - 1) / kAttnWaves));
@@ -1343,19 +1458,23 @@ extern "C" int verify_attention_workspace_size(const verify_attn_params* params,
     if (!bytes) return VERIFY_EINVAL;
     int rc = validate(params, total_q, max_q_len, max_seq_len);
     if (rc != VERIFY_OK) return rc;
-    AttnPlan pl;
+    // enough for verify_attention and verify_attention_append alike
+    AttnPlan pl, pla;
     rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl);
+    if (rc == VERIFY_OK) rc = make_plan(params, total_q, max_q_len, max_seq_len, &pla, true);
     if (rc != VERIFY_OK) return rc;
-    *bytes = pl.total_bytes;
+    *bytes = std::max(pl.total_bytes, pla.total_bytes);
     return VERIFY_OK;
 }
 
-extern "C" int verify_attention(const verify_attn_params* params, int32_t total_q,
-                                int32_t max_q_len, int32_t max_seq_len, const void* q,
-                                const void* k_cache, const void* v_cache,
-                                const int32_t* block_tables, const int32_t* seq_lens,
-                                const int32_t* q_start, const float* sinks, void* out,
-                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+namespace {
+
+// verify_attention, and with k_new / v_new non-null verify_attention_append
+int attention_call(const verify_attn_params* params, int32_t total_q, int32_t max_q_len,
+                   int32_t max_seq_len, const void* q, const void* k_cache, const void* v_cache,
+                   const int32_t* block_tables, const int32_t* seq_lens, const int32_t* q_start,
+                   const float* sinks, void* out, void* workspace, size_t workspace_bytes,
+                   const void* k_new, const void* v_new, hipStream_t stream) {
     int rc = validate(params, total_q, max_q_len, max_seq_len);
     if (rc != VERIFY_OK) return rc;
     const verify_attn_params& p = *params;
@@ -1365,7 +1484,7 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
     // at least one block
     if (total_q > 0 && p.num_blocks < 1) return VERIFY_EINVAL;
     AttnPlan pl;
-    rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl);
+    rc = make_plan(params, total_q, max_q_len, max_seq_len, &pl, k_new != nullptr);
     if (rc != VERIFY_OK) return rc;
     if (workspace_bytes < pl.total_bytes || (pl.total_bytes > 0 && !workspace)) return VERIFY_EWORKSPACE;
     if (p.num_seqs == 0 || total_q == 0) return VERIFY_OK;
@@ -1380,6 +1499,8 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
         m.seq_lens = seq_lens;
         m.q_start = q_start;
         m.out = static_cast<uint16_t*>(out);
+        m.k_new = static_cast<const uint16_t*>(k_new);
+        m.v_new = static_cast<const uint16_t*>(v_new);
         PArgs a{};
         a.num_seqs = p.num_seqs;
         a.hq = p.num_q_heads;
@@ -1440,9 +1561,37 @@ extern "C" int verify_attention(const verify_attn_params* params, int32_t total_
     a.max_splits = pl.max_splits;
     a.row_groups = pl.row_groups;
     a.sinks = sinks;
+    a.k_new = k_new;
+    a.v_new = v_new;
     if (p.head_dim == 128) launch_valu<float, 128>(a, pl, total_q, stream);
     else launch_valu<float, 64>(a, pl, total_q, stream);
     return check_launch();
+}
+
+}  // namespace
+
+extern "C" int verify_attention(const verify_attn_params* params, int32_t total_q,
+                                int32_t max_q_len, int32_t max_seq_len, const void* q,
+                                const void* k_cache, const void* v_cache,
+                                const int32_t* block_tables, const int32_t* seq_lens,
+                                const int32_t* q_start, const float* sinks, void* out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return attention_call(params, total_q, max_q_len, max_seq_len, q, k_cache, v_cache,
+                          block_tables, seq_lens, q_start, sinks, out, workspace, workspace_bytes,
+                          nullptr, nullptr, stream);
+}
+
+extern "C" int verify_attention_append(const verify_attn_params* params, int32_t total_q,
+                                       int32_t max_q_len, int32_t max_seq_len, const void* q,
+                                       const void* k_new, const void* v_new, void* k_cache,
+                                       void* v_cache, const int32_t* block_tables,
+                                       const int32_t* seq_lens, const int32_t* q_start,
+                                       const float* sinks, void* out, void* workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
+    if (total_q > 0 && (!k_new || !v_new)) return VERIFY_EINVAL;
+    return attention_call(params, total_q, max_q_len, max_seq_len, q, k_cache, v_cache,
+                          block_tables, seq_lens, q_start, sinks, out, workspace, workspace_bytes,
+                          total_q > 0 ? k_new : nullptr, total_q > 0 ? v_new : nullptr, stream);
 }
 
 extern "C" int verify_attention_plan(const verify_attn_params* params, int32_t total_q,

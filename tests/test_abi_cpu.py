@@ -30,7 +30,8 @@ def test_header_declares_the_entry_points():
     for n in ("verify_attention", "verify_accept", "verify_accept_sampled", "verify_budget",
               "verify_kv_append", "verify_attention_workspace_size",
               "verify_accept_workspace_size", "verify_lmhead_accept", "verify_accept_noalloc",
-              "verify_lmhead_accept_workspace_size", "verify_check_batch", "verify_status_string",
+              "verify_lmhead_accept_workspace_size", "verify_check_batch", "verify_attention_append",
+              "verify_status_string",
               "verify_abi_version"):
         assert n in names
 
@@ -39,7 +40,7 @@ def test_library_exports_every_declared_symbol():
     lib = av.library()
     for name in declared_symbols():
         assert hasattr(lib, name), name
-    assert av.abi_version() == 10700
+    assert av.abi_version() == 10800
     assert lib.verify_status_string(0) == b"ok"
     assert lib.verify_status_string(-3) == b"workspace too small"
 
@@ -250,6 +251,26 @@ def test_budget_argument_validation():
     assert call(cx=d) == av.EINVAL                    # ctx_len without seq_lens
     assert call(sl=d) == av.EINVAL                    # seq_lens without ctx_len
     assert call(num_seqs=1 << 20, max_len=4096, cap=1 << 40) == av.EUNSUPPORTED
+
+
+def test_attention_append_argument_validation():
+    """verify_attention_append: verify_attention's checks, and the new tokens'
+    arrays are required once there are rows."""
+    lib = av.library()
+    d = ctypes.c_void_p(0x1000)
+    sz = ctypes.c_size_t(1 << 30)
+    args = lambda kn, vn: (ctypes.byref(_params()), 36, 9, 1000, d, kn, vn, d, d, d, d, d, None, d, d,
+                           sz, None)
+    assert lib.verify_attention_append(*args(None, d)) == av.EINVAL
+    assert lib.verify_attention_append(*args(d, None)) == av.EINVAL
+    bad = (ctypes.byref(_params(head_dim=96)), 36, 9, 1000, d, d, d, d, d, d, d, d, None, d, d, sz, None)
+    assert lib.verify_attention_append(*bad) == av.EUNSUPPORTED
+    small = (ctypes.byref(_params()), 36, 9, 1000, d, d, d, d, d, d, d, d, None, d, d,
+             ctypes.c_size_t(0), None)
+    assert lib.verify_attention_append(*small) == av.EWORKSPACE
+    # no rows: nothing to enqueue, and no q / K / V arrays needed
+    none = (ctypes.byref(_params(num_seqs=0)), 0, 0, 0) + (None,) * 10 + (d, sz, None)
+    assert lib.verify_attention_append(*none) == 0
 
 
 def test_kv_append_argument_validation():

@@ -289,3 +289,48 @@ def test_budget_guards():
     outputs = {k: (t, t.numel()) for k, t in out.items() if k != "tokens"}
     outputs["tokens"] = (out["tokens"], used)
     _twice(call, arena, inputs, outputs, "budget")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_attention_append_guards(dtype):
+    """The fused append: caches, output and workspace guarded; both calls
+    start from the same cache, with different garbage in the output and the
+    workspace, and must agree bit for bit."""
+    p = random_paged(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=dtype,
+                     contexts=[700, 40, 1500, 3000, 9, 260], drafts=[11, 12, 0, 32, 20, 3], seed=14)
+    say("guards attention append", dtype)
+    tdt = p.q.dtype
+    g = torch.Generator().manual_seed(4)
+    T = p.total_q
+    k_new = torch.randn((T, p.Hkv, p.D), generator=g).to(tdt).to(DEV)
+    v_new = torch.randn((T, p.Hkv, p.D), generator=g).to(tdt).to(DEV)
+    q = p.q.to(DEV)
+    bt = torch.as_tensor(p.block_tables, device=DEV)
+    sl = torch.as_tensor(p.seq_lens, device=DEV)
+    qs = torch.as_tensor(p.q_start, device=DEV)
+    mq, ms = int(np.diff(p.q_start).max()), int(p.seq_lens.max())
+    arena = Arena()
+    kc = arena.take("k_cache", tuple(p.k_cache.shape), tdt)
+    vc = arena.take("v_cache", tuple(p.v_cache.shape), tdt)
+    out = arena.take("out", tuple(q.shape), tdt)
+    nbytes = av.attention_workspace_size(q, kc, bt, max_q_len=mq, max_seq_len=ms)
+    ws = arena.take("workspace", (max(nbytes, 1),), torch.uint8)
+    kc0, vc0 = p.k_cache.to(DEV), p.v_cache.to(DEV)
+    inputs = [q, k_new, v_new, bt, sl, qs, kc0, vc0]
+    before = _snapshot(inputs)
+    results = []
+    for out_byte, ws_byte in ((0xA5, 0x5A), (0x5A, 0xFF)):
+        arena.fill(out_byte)
+        for name, raw, n in arena.bufs:
+            if name == "workspace":
+                raw[PAD:PAD + n].fill_(ws_byte)
+        kc.copy_(kc0)
+        vc.copy_(vc0)
+        av.verify_attention_append(q, k_new, v_new, kc, vc, bt, sl, qs, max_q_len=mq, max_seq_len=ms,
+                                   out=out, workspace=ws)
+        arena.check("attention append " + dtype)
+        results.append([_bytes(t).clone() for t in (kc, vc, out)])
+    _assert_unchanged(inputs, before, "attention append " + dtype)
+    for a_, b_ in zip(*results):
+        assert torch.equal(a_, b_)
+    assert not torch.equal(results[0][0], _bytes(kc0))   # the append wrote something
