@@ -195,7 +195,8 @@ def graph_time_us(fn, steps: int) -> float:
 def kv_append_timing(av, bt, steps: int):
     """Device time of writing the step's new tokens' K/V ([T, Hkv, D] each)
     into the first layer's cache (verify_kv_append), and its bytes: the new
-    K/V read once and written once.  The calls rotate over enough copies of
+    K/V read once and written once; and the append fused into the attention
+    launch (verify_attention_append) against the append then the attention.  The calls rotate over enough copies of
     the new K/V (more than the 256 MB Infinity Cache holds) that every call
     reads its inputs from HBM."""
     import torch
@@ -221,9 +222,49 @@ def kv_append_timing(av, bt, steps: int):
     fn()
     us = graph_time_us(fn, max(steps, 2 * copies))
     nbytes = 2 * one
-    del kc, vc, ks, vs
+
+    # the append fused into the attention launch (verify_attention_append)
+    # against the append followed by the attention, on the same cache copy:
+    # mean call time over `steps` calls with events at the ends, the two
+    # alternated over three rounds, the last round reported
+    kw = dict(max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len, sliding_window=l.window,
+              sinks=l.sinks)
+    out = torch.empty_like(l.q)
+    ws = torch.empty(max(1, av.attention_workspace_size(l.q, kc, bt.t_block_tables, max_q_len=bt.max_q_len,
+                                                        max_seq_len=bt.max_seq_len,
+                                                        sliding_window=l.window)),
+                     dtype=torch.uint8, device=l.q.device)
+
+    def two():
+        c = it[0] % copies
+        it[0] += 1
+        av.verify_kv_append(ks[c], vs[c], kc, vc, bt.t_block_tables, bt.t_seq_lens, bt.t_q_start)
+        av.verify_attention(l.q, kc, vc, bt.t_block_tables, bt.t_seq_lens, bt.t_q_start, out=out,
+                            workspace=ws, **kw)
+
+    def fused():
+        c = it[0] % copies
+        it[0] += 1
+        av.verify_attention_append(l.q, ks[c], vs[c], kc, vc, bt.t_block_tables, bt.t_seq_lens,
+                                   bt.t_q_start, out=out, workspace=ws, **kw)
+
+    def events_us(f):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps
+
+    for _ in range(3):
+        t_two, t_fused = events_us(two), events_us(fused)
+    del kc, vc, ks, vs, out, ws
     return {"us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rows": T,
-            "input_copies": copies}
+            "input_copies": copies, "append_then_attention_us": t_two,
+            "fused_attention_append_us": t_fused}
 
 
 def accept_timing(av, bt, steps: int, aws):
