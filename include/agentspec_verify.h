@@ -179,6 +179,8 @@ int verify_attention_append(const verify_attn_params *params, int32_t total_q, i
 /*
  * verify_attention_plan -- the work decomposition verify_attention would use
  * for the same arguments, for tests and tools (nothing is launched).
+ * verify_attention_append may launch fewer persistent workgroups where its
+ * kernel fits fewer per compute unit; it is not described here.
  *
  *   info     int32[VERIFY_ATTN_PLAN_INFO], written in full (unused entries 0)
  *   info[0]  1: bf16 persistent MFMA schedule, 0: fp32 split-K VALU kernel
