@@ -225,8 +225,9 @@ def kv_append_timing(av, bt, steps: int):
 
     # the append fused into the attention launch (verify_attention_append)
     # against the append followed by the attention, on the same cache copy:
-    # mean call time over `steps` calls with events at the ends, the two
-    # alternated over three rounds, the last round reported
+    # `steps` calls of each captured in a HIP graph and replayed (device time,
+    # without the host's launch cost), the two alternated over two rounds, the
+    # last round reported
     kw = dict(max_q_len=bt.max_q_len, max_seq_len=bt.max_seq_len, sliding_window=l.window,
               sinks=l.sinks)
     out = torch.empty_like(l.q)
@@ -248,19 +249,10 @@ def kv_append_timing(av, bt, steps: int):
         av.verify_attention_append(l.q, ks[c], vs[c], kc, vc, bt.t_block_tables, bt.t_seq_lens,
                                    bt.t_q_start, out=out, workspace=ws, **kw)
 
-    def events_us(f):
-        f()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(steps):
-            f()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / steps
-
-    for _ in range(3):
-        t_two, t_fused = events_us(two), events_us(fused)
+    two()
+    fused()
+    for _ in range(2):
+        t_two, t_fused = graph_time_us(two, steps), graph_time_us(fused, steps)
     del kc, vc, ks, vs, out, ws
     return {"us": us, "bytes": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9, "rows": T,
             "input_copies": copies, "append_then_attention_us": t_two,
@@ -513,11 +505,12 @@ def cpu_baseline(bt, budget_s: float):
 
 def summarize_trace(csv_path: str, layers: int) -> None:
     """Inter-kernel idle time inside the timed verify steps, from the kernel
-    trace of a rocprofv3 --kernel-trace run of bench.py.  A step is the
-    sequence (attn_persist, attn_combine_slots) x layers, argmax_chunks,
-    accept_scan issued back to back; every such run of steps in the trace is
-    used (the timed steps and the warm-up steps have this form; the
-    attention-only calls timed after them do not)."""
+    trace of a rocprofv3 --kernel-trace run of bench.py.  A step is a run of
+    attention kernels (per layer and row class: attn_schedule for large
+    batches, attn_persist, attn_combine_slots; at least two per layer) ended by
+    argmax_chunks, accept_scan, issued back to back.  The most frequent such
+    kernel sequence is the step (the timed steps and the warm-up steps have
+    it; the attention-only calls timed after them do not)."""
     import collections
     import csv
     import re
@@ -528,17 +521,20 @@ def summarize_trace(csv_path: str, layers: int) -> None:
         name = m.group(1) if m else "other"
         rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), name))
     rows.sort()
-    sig = ["attn_persist", "attn_combine_slots"] * layers + ["argmax_chunks", "accept_scan"]
-    steps = []
-    i = 0
-    while i + len(sig) <= len(rows):
-        if [x[2] for x in rows[i:i + len(sig)]] == sig:
-            steps.append(rows[i:i + len(sig)])
-            i += len(sig)
-        else:
-            i += 1
-    if not steps:
+    names = [x[2] for x in rows]
+    attention = {"attn_schedule", "attn_persist", "attn_combine_slots"}
+    found = []
+    for j in range(len(rows) - 1):
+        if names[j] == "argmax_chunks" and names[j + 1] == "accept_scan":
+            k = j
+            while k > 0 and names[k - 1] in attention:
+                k -= 1
+            if j - k >= 2 * layers:
+                found.append((k, j + 2))
+    if not found:
         raise SystemExit("no verify step found in %s" % csv_path)
+    sig = list(collections.Counter(tuple(names[a:b]) for a, b in found).most_common(1)[0][0])
+    steps = [rows[a:b] for a, b in found if names[a:b] == sig]
     dur = collections.defaultdict(list)
     gaps = collections.defaultdict(list)
     spans, busy, between = [], [], []
