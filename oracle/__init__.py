@@ -60,7 +60,7 @@ def _load():
     i32, i64, f64, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
     lib.oracle_kv_append.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.oracle_kv_append.restype = ctypes.c_int
-    lib.oracle_attention.argtypes = [i32, i32, i32, i32, i32, i32, f64, i32, vp, vp, vp, vp,
+    lib.oracle_attention.argtypes = [i32, i32, i32, i32, i32, i32, i32, f64, i32, vp, vp, vp, vp,
                                      vp, vp, i64, vp, vp, vp, vp]
     lib.oracle_attention.restype = ctypes.c_int
     lib.oracle_argmax.argtypes = [i64, i64, i64, i32, vp, vp, vp]
@@ -137,8 +137,9 @@ def attention(*, num_q_heads: int, num_kv_heads: int, head_dim: int, sliding_win
     sk = None if sinks is None else np.ascontiguousarray(sinks, dtype=np.float64)
     if sk is not None and sk.shape != (num_q_heads,):
         raise ValueError("sinks must have one entry per query head")
+    num_blocks = k_cache.size // (num_kv_heads * head_dim * 16)
     rc = lib.oracle_attention(num_seqs, num_q_heads, num_kv_heads, head_dim, bt.shape[1],
-                              sliding_window, float(scale), dtype, _ptr(q), _ptr(k_cache),
+                              num_blocks, sliding_window, float(scale), dtype, _ptr(q), _ptr(k_cache),
                               _ptr(v_cache), _ptr(bt), _ptr(sl), _ptr(qs), rows.shape[0],
                               _ptr(rows), _ptr(heads), _ptr(sk) if sk is not None else None,
                               _ptr(out))

@@ -42,7 +42,10 @@
  *   - query head h reads KV head floor(h / (Hq / Hkv)) (grouped-query);
  *   - scale defaults to 1/sqrt(head_dim); no soft-cap, no bias; attention
  *     sinks only when given (see oracle_attention);
- *   - a row with no visible key (only possible when S < n) yields zeros.
+ *   - a row with no visible key (only possible when S < n) yields zeros;
+ *   - a key whose block id lies outside [0, num_blocks) is not a key at all:
+ *     it takes no part in the softmax (the library's convention for unmapped
+ *     block-table entries), and a row left without keys yields zeros.
  *
  * Paged KV layout read here (element index, x = 16 bytes / element size):
  *   K: [num_blocks][Hkv][D/x][16][x]   -> K[t][d] of physical block b, head g
@@ -93,7 +96,8 @@ static int find_request(int num_seqs, const int32_t *q_start, int32_t row)
  * Returns 0, or -1 on an argument that cannot be interpreted.
  */
 int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
-                     int32_t head_dim, int32_t max_blocks_per_seq, int32_t sliding_window,
+                     int32_t head_dim, int32_t max_blocks_per_seq, int32_t num_blocks,
+                     int32_t sliding_window,
                      double scale, int32_t dtype, const void *q, const void *k_cache,
                      const void *v_cache, const int32_t *block_tables,
                      const int32_t *seq_lens, const int32_t *q_start, int64_t n_pairs,
@@ -131,6 +135,7 @@ int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads
         double smax = -INFINITY;
         for (int64_t t = lo; t <= p; ++t) {
             const int64_t b = block_tables[(int64_t)i * max_blocks_per_seq + t / 16];
+            if (b < 0 || b >= num_blocks) { s[t - lo] = -INFINITY; continue; } /* no key */
             double acc = 0.0;
             for (int d = 0; d < D; ++d) {
                 const double qd = elem_to_double(q, dtype, ((int64_t)row * num_q_heads + h) * D + d);
@@ -145,8 +150,10 @@ int oracle_attention(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads
         const double sink = sinks ? sinks[h] : -INFINITY;
         if (sink > smax) smax = sink;
         double denom = sinks ? exp(sink - smax) : 0.0;
+        if (smax == -INFINITY) { free(s); continue; } /* no key and no sink: zeros */
         for (int64_t t = lo; t <= p; ++t) {
             const int64_t b = block_tables[(int64_t)i * max_blocks_per_seq + t / 16];
+            if (b < 0 || b >= num_blocks) continue;
             const double w = exp(s[t - lo] - smax);
             denom += w;
             for (int d = 0; d < D; ++d) {

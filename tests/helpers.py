@@ -80,9 +80,11 @@ def random_paged(*, num_q_heads, num_kv_heads, head_dim, dtype, contexts, drafts
                  window=window, seed=seed, spare_blocks=spare_blocks)
 
 
-def sdpa_reference(p: Paged) -> np.ndarray:
+def sdpa_reference(p: Paged, missing=None) -> np.ndarray:
     """torch scaled_dot_product_attention (float64, CPU) on the logical tensors, with
-    an explicit boolean mask for the in-draft causal rule and the sliding window."""
+    an explicit boolean mask for the in-draft causal rule and the sliding window.
+    ``missing``: optional {request: set of logical block indices} whose keys are
+    left out of the mask (an unmapped block); a row left with no key is zero."""
     G = p.Hq // p.Hkv
     out = np.zeros((p.total_q, p.Hq, p.D))
     qf = p.q.to(torch.float64)
@@ -94,9 +96,12 @@ def sdpa_reference(p: Paged) -> np.ndarray:
         mask = t <= pos
         if p.window > 0:
             mask &= t > pos - p.window
+        for b in (missing or {}).get(i, ()):
+            mask &= (t // 16) != b
         qi = qf[q0:q1].permute(1, 0, 2)[None]                         # [1, Hq, n, D]
         ki = p.k_logical[i].permute(1, 0, 2).repeat_interleave(G, 0)[None]  # [1, Hq, S, D]
         vi = p.v_logical[i].permute(1, 0, 2).repeat_interleave(G, 0)[None]
         o = torch.nn.functional.scaled_dot_product_attention(qi, ki, vi, attn_mask=mask)
+        o = torch.where(mask.any(dim=1)[None, None, :, None], o, torch.zeros_like(o))
         out[q0:q1] = o[0].permute(1, 0, 2).numpy()
     return out

@@ -38,6 +38,30 @@ def test_attention_matches_sdpa(dtype, hq, hkv, d, window):
     np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("window", [0, 20])
+def test_attention_skips_keys_on_unmapped_blocks(dtype, window):
+    """A key whose block id lies outside [0, num_blocks) is no key: the oracle
+    equals SDPA with those positions masked out, and a row left with no key
+    (request 3's only block) is zero."""
+    p = random_paged(num_q_heads=8, num_kv_heads=2, head_dim=32, dtype=dtype,
+                     contexts=[40, 70, 20, 3], drafts=[5, 9, 0, 4], window=window, seed=31)
+    bt = p.block_tables.copy()
+    bt[0, 1] = -1                      # request 0: positions 16..31
+    bt[1, 0] = p.num_blocks            # request 1: positions 0..15 (past the cache)
+    bt[1, 4] = -3                      # request 1: positions 64..79 (new tokens among them)
+    bt[3, 0] = -1                      # request 3: its only block
+    args = p.oracle_args()
+    args.update(block_tables=bt)
+    got = oracle.attention(**args)
+    ref = sdpa_reference(p, missing={0: {1}, 1: {0, 4}, 3: {0}})
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+    q0, q1 = p.q_start[3], p.q_start[4]
+    assert np.all(got[q0:q1] == 0.0)
+    # the unmapped keys matter: with valid ids the result differs
+    assert not np.allclose(got, run_oracle(p))
+
+
 def _const_keys(S, hkv, d):
     return np.ones((S, hkv, d)) * 0.25
 
