@@ -349,6 +349,40 @@ def test_attention_row_classes(contexts):
         _check_paged(p, split=split, what="row classes split=%d" % split)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("hq,hkv,d,window", [(32, 8, 128, 0), (64, 8, 64, 128), (16, 2, 64, 20)])
+def test_attention_skips_unmapped_blocks(dtype, hq, hkv, d, window):
+    """Block ids outside [0, num_blocks) (negative, or past the cache) hold no
+    keys: every vector against the oracle, which leaves those positions out of
+    the softmax, across split settings; a request whose only block is unmapped
+    gets zeros.  The drafts (up to 32) put the batch in two row classes at
+    head dim 128."""
+    say("attn unmapped blocks", dtype, hq, hkv, d, window)
+    p = random_paged(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                     contexts=[400, 70, 3, 900, 33], drafts=[5, 32, 4, 9, 0], window=window,
+                     seed=hq + d + window)
+    bt = p.block_tables.copy()
+    bt[0, 3] = -1                          # request 0: a block in the middle
+    bt[1, 5] = p.num_blocks + 2            # request 1: the new tokens' last block
+    bt[2, 0] = -1                          # request 2: its only block
+    bt[3, 0] = p.num_blocks                # request 3: the first block
+    bt[3, (int(p.seq_lens[3]) - 1) // 16] = -7   # and the last
+    dv = _to_dev(p)
+    t_bt = torch.as_tensor(bt, device=DEV)
+    args = p.oracle_args()
+    args.update(block_tables=bt)
+    ref = oracle.attention(**args)
+    q0, q1 = p.q_start[2], p.q_start[3]
+    assert np.all(ref[q0:q1] == 0.0)
+    for split in (0, 1, 3):
+        out = gpu_attention(dv["q"], dv["kc"], dv["vc"], t_bt, dv["sl"], dv["qs"],
+                            max_q_len=int(np.diff(p.q_start).max()),
+                            max_seq_len=int(p.seq_lens.max()), window=window, split=split)
+        got = to_host_f64(out)
+        assert_attention_close(got, ref, dtype, "unmapped split=%d" % split)
+        assert np.all(got[q0:q1] == 0.0)
+
+
 SEEDS = range(5)
 EVERY_PAIR = ["qwen3_8b", "dsk_distill_8b", "gpt_oss_20b"]
 
