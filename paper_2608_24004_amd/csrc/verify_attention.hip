@@ -633,8 +633,13 @@ __device__ __forceinline__ bool block_needs_mask(int b, int p_first, int S, int 
 // Global->LDS loads need about sixteen wavefronts per compute unit to reach
 // full HBM bandwidth, so one-tile configurations are held to four waves per
 // SIMD (at most 128 registers each).
-template <int TPW>
-constexpr int persist_waves_per_eu() { return TPW == 1 ? 4 : 2; }
+// Waves per SIMD the persistent kernel is built for.  The fused append's
+// four-wavefront kernel is held to three, the residency of the plain one: its
+// patch would otherwise take it to 192 registers and two workgroups per
+// compute unit (long-context fused call 9.27 -> 8.66 ms); the few values it
+// then keeps in scratch are reloaded only on pair switches and patched blocks.
+template <int TPW, int NW = 1, bool APPEND = false>
+constexpr int persist_waves_per_eu() { return TPW == 1 ? 4 : (APPEND && NW == 4 && TPW == 2 ? 3 : 2); }
 
 // APPEND: the fused KV append (verify_attention_append).  The request's new
 // tokens, positions S_i - n_i .. S_i - 1 of rows q_start[i] .. q_start[i+1]-1,
@@ -645,7 +650,7 @@ constexpr int persist_waves_per_eu() { return TPW == 1 ? 4 : 2; }
 // ordering between workgroups is needed.
 template <int D, int NW, int TPW, int PD, bool APPEND>
 __global__ __launch_bounds__(NW * kWave)
-__attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW>()))) void attn_persist(
+__attribute__((amdgpu_waves_per_eu(persist_waves_per_eu<TPW, NW, APPEND>()))) void attn_persist(
     PArgs a, const uint16_t* __restrict__ qg, const uint8_t* __restrict__ kcg,
     const uint8_t* __restrict__ vcg, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ q_start,
