@@ -45,6 +45,25 @@ def test_library_exports_every_declared_symbol():
     assert lib.verify_status_string(-3) == b"workspace too small"
 
 
+def test_binding_constants_match_the_header():
+    """The binding's copies of the header's constants and enum values."""
+    src = open(os.path.join(ROOT, "include", "agentspec_verify.h")).read()
+    defs = {m.group(1): m.group(2).strip() for m in re.finditer(r"#define\s+(VERIFY_\w+)\s+([^\n]+)", src)}
+    assert int(defs["VERIFY_ATTN_PLAN_INFO"]) == av.PLAN_INFO
+    assert int(defs["VERIFY_CHECK_COUNTS"]) == av.CHECK_COUNTS == len(av.CHECK_KINDS) + 1
+    m = re.fullmatch(r"\(\s*(\d+)u?\s*<<\s*(\d+)\s*\)", defs["VERIFY_NOALLOC_SCRATCH_BYTES"])
+    assert m and int(m.group(1)) << int(m.group(2)) == av.NOALLOC_SCRATCH_BYTES
+    order = ["VERIFY_CHECK_ROWS", "VERIFY_CHECK_QLEN", "VERIFY_CHECK_SHORT", "VERIFY_CHECK_LONG",
+             "VERIFY_CHECK_BLOCK_ID"]
+    assert [int(defs[k]) for k in order] == list(range(len(av.CHECK_KINDS)))
+    assert int(defs["VERIFY_CHECK_FIRST"]) == len(av.CHECK_KINDS)
+    enums = dict(re.findall(r"(VERIFY_E?\w+)\s*=\s*(-?\d+)", src))
+    assert (int(enums["VERIFY_OK"]), int(enums["VERIFY_EINVAL"]), int(enums["VERIFY_EUNSUPPORTED"]),
+            int(enums["VERIFY_EWORKSPACE"]), int(enums["VERIFY_EHIP"])) == (
+        av.OK, av.EINVAL, av.EUNSUPPORTED, av.EWORKSPACE, av.EHIP)
+    assert (int(enums["VERIFY_F32"]), int(enums["VERIFY_BF16"])) == (av.F32, av.BF16)
+
+
 def test_missing_library_fails_loudly(tmp_path):
     with pytest.raises(RuntimeError, match="not built"):
         av.library(str(tmp_path / "nope.so"))
