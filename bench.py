@@ -119,22 +119,32 @@ def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
     import csv
     import re
 
+    # the kernels one verify_attention call launches (the append is a separate
+    # call).  A call launches each of them once per row class and layer, with a
+    # grid of its own, so they are told apart by template arguments and grid;
+    # the fused append's kernels (a side call) are not part of it.
+    call_kernels = ("attn_schedule", "attn_persist", "attn_combine_slots", "attn_valu", "attn_combine")
+
     def per_kernel(path, counter):
         by_dispatch = collections.defaultdict(float)
-        names = {}
+        names, grids = {}, {}
         for r in csv.DictReader(open(path)):
             if r["Counter_Name"] != counter:
                 continue
             d = r["Dispatch_Id"]
             by_dispatch[d] += float(r["Counter_Value"])
             names[d] = r["Kernel_Name"]
+            grids[d] = r.get("Grid_Size", "")
         groups = collections.defaultdict(list)
         calib = None
         for d in sorted(by_dispatch, key=int):
             n = names[d]
-            m = re.search(r"averify::\(anonymous namespace\)::(\w+)", n)
+            m = re.search(r"averify::\(anonymous namespace\)::(\w+)(<[^>]*>)?", n)
             if m:
-                groups[m.group(1)].append(by_dispatch[d])
+                key = m.group(1)
+                if key in call_kernels:
+                    key = "%s%s grid %s" % (key, (m.group(2) or "").replace(" ", ""), grids[d])
+                groups[key].append(by_dispatch[d])
             elif "bitwise_not" in n:
                 calib = by_dispatch[d]
         return {k: sum(v) / len(v) for k, v in groups.items()}, \
@@ -146,19 +156,17 @@ def summarize_pmc(fetch_csv: str, write_csv: str, workload: str) -> None:
         raise SystemExit("no calibration dispatch (run bench.py with --copy-calibration)")
     ff = CALIB_BYTES / (fcal * 1024.0)
     wf = CALIB_BYTES / (wcal * 1024.0)
-    # the kernels one verify_attention call launches (the append is a separate call)
-    call_kernels = ("attn_schedule", "attn_persist", "attn_combine_slots", "attn_valu", "attn_combine")
-    attn = [k for k in fk if k in call_kernels]
+    attn = [k for k in fk if k.split("<")[0].split(" ")[0] in call_kernels and ",true>" not in k]
     total = 0.0
     lines = []
     for k in sorted(attn):
         fb = fk[k] * 1024.0 * ff
         wb = wk.get(k, 0.0) * 1024.0 * wf
         total += fb + wb
-        lines.append("  %-22s dispatches %3d  FETCH %10.1f KiB  WRITE %9.1f KiB  -> %.4f GB read, "
+        lines.append("  %-48s dispatches %3d  FETCH %10.1f KiB  WRITE %9.1f KiB  -> %.4f GB read, "
                      "%.4f GB written" % (k, fn[k], fk[k], wk.get(k, 0.0), fb / 1e9, wb / 1e9))
     for k in sorted(set(fk) - set(attn)):
-        lines.append("  %-22s dispatches %3d  FETCH %10.1f KiB  WRITE %9.1f KiB  (not attention)" % (
+        lines.append("  %-48s dispatches %3d  FETCH %10.1f KiB  WRITE %9.1f KiB  (not this call)" % (
             k, fn[k], fk[k], wk.get(k, 0.0)))
     print("workload: %s" % workload)
     print("source_sha256: %s" % kernel_source_hash())
