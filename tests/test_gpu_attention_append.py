@@ -23,7 +23,7 @@ import torch
 import oracle
 import paper_2608_24004_amd as av
 import workload
-from gpu_common import assert_attention_close, rel_err_rows, to_host_f64
+from gpu_common import assert_attention_close, rel_err_rows, row_reach, to_host_f64
 from helpers import random_paged
 
 pytestmark = pytest.mark.gpu
@@ -171,3 +171,46 @@ def test_fused_append_full_size(name):
         say("  window", layer.window, "max rel err vs append + attention %.2e" % err.max(),
             "bitwise", torch.equal(_bits(out), _bits(ref)))
         assert float(err.max()) <= 2e-2
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fused_append_writes_every_new_token_past_max_q_len(dtype):
+    """A request with more rows than max_q_len promised: the rows past the
+    launch's reach are NaN, as in verify_attention, but the append still
+    stores every new token (the walk covers all of the request's blocks)."""
+    say("attention append past max_q_len", dtype)
+    p = random_paged(num_q_heads=32, num_kv_heads=8, head_dim=128, dtype=dtype,
+                     contexts=[300, 600, 50], drafts=[40, 2, 7], seed=41)
+    code = workload.dtype_code(dtype)
+    k_new, v_new = _new_kv(p.total_q, p.Hkv, p.D, dtype, seed=3)
+    kc_ref, vc_ref = oracle.kv_append(num_kv_heads=p.Hkv, head_dim=p.D, dtype=code,
+                                      k_new=workload.host_storage(k_new),
+                                      v_new=workload.host_storage(v_new),
+                                      block_tables=p.block_tables, seq_lens=p.seq_lens,
+                                      q_start=p.q_start, k_cache=workload.host_storage(p.k_cache),
+                                      v_cache=workload.host_storage(p.v_cache))
+    d = lambda a: torch.as_tensor(a, device=DEV)
+    q, kc, vc = p.q.to(DEV), p.k_cache.to(DEV), p.v_cache.to(DEV)
+    mq = 4
+    out = av.verify_attention_append(q, k_new.to(DEV), v_new.to(DEV), kc, vc, d(p.block_tables),
+                                     d(p.seq_lens), d(p.q_start), max_q_len=mq,
+                                     max_seq_len=int(p.seq_lens.max()))
+    torch.cuda.synchronize()
+    assert np.array_equal(workload.host_storage(kc), kc_ref)
+    assert np.array_equal(workload.host_storage(vc), vc_ref)
+    args = p.oracle_args()
+    args.update(k_cache=kc_ref, v_cache=vc_ref)
+    ref = oracle.attention(**args)
+    got = to_host_f64(out)
+    plan = av.attention_plan(q, kc, d(p.block_tables), max_q_len=mq, max_seq_len=int(p.seq_lens.max()))
+    G = p.Hq // p.Hkv
+    reached = np.zeros(got.shape[:2], dtype=bool)
+    for i in range(len(p.seq_lens)):
+        q0, q1 = int(p.q_start[i]), int(p.q_start[i + 1])
+        reach = row_reach(plan, G * (q1 - q0))
+        for j in range(q1 - q0):
+            for h in range(p.Hq):
+                reached[q0 + j, h] = j * G + h % G < reach
+    assert not reached.all()
+    assert np.isnan(got[~reached]).all()
+    assert_attention_close(got[reached], ref[reached], dtype, "reached rows")
